@@ -1,0 +1,354 @@
+#!/usr/bin/env python3
+"""Restore+verify throughput of one GPU's engine state (libgms on MI355X).
+
+A step is one fused restore+verify of the Llama-style 8B bf16 weight set
+(291 tensors, 16.06 GB) from a device-resident packed image: every tensor is
+rewritten from the image and every 4 KiB block is hashed in registers and
+compared with the hashes recorded at snapshot time.  ``value`` is payload
+bytes restored and verified per second (GB/s, 1e9).  The same run also
+measures the other rows of the path (snapshot, plain restore, verify alone,
+pinned-host restore through the staging ring and zero-copy, the 8 GiB KV pool
+with live-block restore and a planted corruption), the host-link and plain
+copy references, the roofline of the fused restore kernel and the CPU oracle
+on a bounded sample.  Prints one JSON line on stdout; progress goes to stderr.
+
+    python bench.py [--gpus 1] [--steps 20] [--warmup 3] [--rows all|main,cpu,...]
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import statistics
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "restore+verify GB/s on 1 GPU; seconds to restore a 16 GB weight shard"
+HBM_PEAK_GBS = 8000.0
+ALL_ROWS = ["main", "snapshot", "plain", "verify", "h2d", "kv", "copy", "cpu"]
+KERNEL_SOURCES = ["paper_2609_25451_amd/csrc/gms_kernels.hip", "paper_2609_25451_amd/csrc/gms_internal.h"]
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_restore_verify_llama8b.json")
+
+
+def log(*a):
+    print("[bench]", *a, file=sys.stderr, flush=True)
+
+
+def kernel_source_digest() -> str:
+    h = hashlib.sha256()
+    for p in KERNEL_SOURCES:
+        with open(os.path.join(ROOT, p), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--rows", default="all", help="comma list of " + ",".join(ALL_ROWS) + " or 'all'")
+    ap.add_argument("--calib-copy", action="store_true",
+                    help="also run one plain 1 GiB torch copy (counter calibration)")
+    return ap.parse_args()
+
+
+class Timer:
+    """HIP events on the stream the library launches on (torch's current stream)."""
+
+    def __init__(self, torch):
+        self.torch = torch
+
+    def run(self, fn, reps: int):
+        t = self.torch
+        s = t.cuda.current_stream()
+        out = []
+        for _ in range(reps):
+            a, b = t.cuda.Event(enable_timing=True), t.cuda.Event(enable_timing=True)
+            a.record(s)
+            fn()
+            b.record(s)
+            b.synchronize()
+            out.append(a.elapsed_time(b) / 1e3)
+        return out
+
+
+def build_weights(torch, synth, name):
+    seed, specs = synth.weight_set(name)
+    tensors = []
+    for i, sp in enumerate(specs):
+        t = torch.empty(sp.shape, dtype=torch.bfloat16, device="cuda")
+        synth.dev_fill_bf16(t.data_ptr(), t.numel(), seed, i)
+        tensors.append(t)
+    torch.cuda.synchronize()
+    return seed, specs, tensors
+
+
+def main():
+    args = parse()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
+        print("bench.py measures one GPU only: the restore path is per-GPU and independent "
+              "(each rank restores its own shard); run with --gpus 1", file=sys.stderr)
+        sys.exit(2)
+    rows = ALL_ROWS if args.rows == "all" else [r.strip() for r in args.rows.split(",") if r.strip()]
+
+    import numpy as np
+    import torch
+
+    import paper_2609_25451_amd as gms
+    import synth
+
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        sys.exit(1)
+    torch.cuda.set_device(0)
+    timer = Timer(torch)
+    result_rows = {}
+
+    # ---------------------------------------------------------------- workload
+    t0 = time.time()
+    seed, specs, tensors = build_weights(torch, synth, "llama8b")
+    m = gms.Manifest(tensors, device=0)
+    P, nb, n = m.payload_bytes, m.num_blocks, m.num_entries
+    image = torch.empty(m.image_bytes, dtype=torch.uint8, device="cuda")
+    expected = torch.zeros(nb, dtype=torch.int64, device="cuda")
+    ten_hash = torch.zeros(n, dtype=torch.int64, device="cuda")
+    gms.snapshot(m, image, m.image_bytes, gms.MEM_DEVICE, blk_hash=expected, ten_hash=ten_hash)
+    torch.cuda.synchronize()
+    log(f"llama8b: {n} tensors, {P} B, {nb} blocks, {m.num_chunks} chunks; setup {time.time() - t0:.1f}s")
+
+    cnt = torch.zeros(1, dtype=torch.int64, device="cuda")
+    mlist = torch.zeros(64, dtype=torch.int64, device="cuda")
+
+    def fused_restore():
+        gms.restore(m, image, m.image_bytes, gms.MEM_DEVICE, expected=expected, mismatch_count=cnt,
+                    mismatch_list=mlist, mismatch_cap=64)
+
+    # correctness gate for the timed configuration: poison, restore, compare a sample
+    for t in tensors:
+        t.view(torch.uint8).fill_(0xA5)
+    fused_restore()
+    torch.cuda.synchronize()
+    assert int(cnt.item()) == 0, "fused restore reported mismatches on a clean image"
+    for i in (0, 1, 7, len(tensors) - 1):
+        k = min(tensors[i].numel(), 1 << 16)
+        got = tensors[i].reshape(-1)[:k].view(torch.int16).cpu().numpy().view(np.uint16)
+        assert np.array_equal(got, synth.bf16_bits(k, seed, i)), f"tensor {i} restored wrong"
+
+    # ---------------------------------------------------------------- main step
+    main_times = []
+    if "main" in rows:
+        for _ in range(args.warmup):
+            fused_restore()
+        torch.cuda.synchronize()
+        s = torch.cuda.current_stream()
+        evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+               for _ in range(args.steps)]
+        torch.cuda.synchronize()
+        w0 = time.perf_counter()
+        for a, b in evs:
+            a.record(s)
+            fused_restore()
+            b.record(s)
+        torch.cuda.synchronize()
+        wall = time.perf_counter() - w0
+        main_times = [a.elapsed_time(b) / 1e3 for a, b in evs]
+        assert int(cnt.item()) == 0
+        log(f"fused restore+verify: wall {wall * 1e3 / args.steps:.3f} ms/step, "
+            f"kernel avg {statistics.mean(main_times) * 1e3:.3f} ms")
+    else:
+        wall = float("nan")
+
+    # ---------------------------------------------------------------- other rows
+    if "snapshot" in rows:
+        blk2 = torch.zeros(nb, dtype=torch.int64, device="cuda")
+        ts = timer.run(lambda: gms.snapshot(m, image, m.image_bytes, gms.MEM_DEVICE, blk_hash=blk2), 5)
+        assert torch.equal(blk2, expected)
+        t = statistics.median(ts)
+        result_rows["snapshot_d2d_hash"] = {"s": t, "GB_s": P / t / 1e9, "hbm_frac": 2 * P / t / 1e9 / HBM_PEAK_GBS}
+    if "plain" in rows:
+        ts = timer.run(lambda: gms.restore(m, image, m.image_bytes, gms.MEM_DEVICE), 5)
+        t = statistics.median(ts)
+        result_rows["restore_d2d_plain"] = {"s": t, "GB_s": P / t / 1e9, "hbm_frac": 2 * P / t / 1e9 / HBM_PEAK_GBS}
+    if "verify" in rows:
+        vc = torch.zeros(1, dtype=torch.int64, device="cuda")
+        ts = timer.run(lambda: gms.verify(m, expected=expected, mismatch_count=vc), 5)
+        assert int(vc.item()) == 0
+        t = statistics.median(ts)
+        result_rows["verify_only"] = {"s": t, "GB_s": P / t / 1e9, "hbm_frac": P / t / 1e9 / HBM_PEAK_GBS}
+    if "copy" in rows:
+        a = torch.empty(4 << 30, dtype=torch.uint8, device="cuda")
+        b = torch.empty_like(a)
+        ts = timer.run(lambda: b.copy_(a), 5)
+        t = statistics.median(ts)
+        result_rows["torch_copy_4GiB_reference"] = {"s": t, "hbm_GB_s": 2 * a.numel() / t / 1e9,
+                                                    "hbm_frac": 2 * a.numel() / t / 1e9 / HBM_PEAK_GBS}
+        del a, b
+    if args.calib_copy:
+        a = torch.ones(1 << 30, dtype=torch.uint8, device="cuda")
+        b = torch.empty_like(a)
+        b.copy_(a)
+        torch.cuda.synchronize()
+        del a, b
+
+    if "h2d" in rows:
+        t0 = time.time()
+        pinned = torch.empty(m.image_bytes, dtype=torch.uint8, pin_memory=True)
+        log(f"pinned {m.image_bytes} B in {time.time() - t0:.1f}s")
+        # link peak: 1 GiB pinned -> device copies
+        gib = pinned[: 1 << 30]
+        dst = torch.empty(1 << 30, dtype=torch.uint8, device="cuda")
+        lt = timer.run(lambda: dst.copy_(gib, non_blocking=True), 10)
+        link = (1 << 30) / statistics.median(lt) / 1e9
+        del dst
+        ts = timer.run(lambda: gms.snapshot(m, pinned, m.image_bytes, gms.MEM_HOST_PINNED), 2)
+        snap_h = statistics.median(ts)
+        hc = torch.zeros(1, dtype=torch.int64, device="cuda")
+
+        def h2d():
+            gms.restore(m, pinned, m.image_bytes, gms.MEM_HOST_PINNED, expected=expected, mismatch_count=hc)
+
+        th = statistics.median(timer.run(h2d, 3))
+        assert int(hc.item()) == 0
+        m.set_staging(0, 0)
+        tz = statistics.median(timer.run(h2d, 2))
+        assert int(hc.item()) == 0
+        m.set_staging(64 << 20, 4)
+        result_rows["h2d"] = {
+            "link_peak_GB_s": link,
+            "restore_verify_ring_s": th, "restore_verify_ring_GB_s": P / th / 1e9,
+            "link_frac": P / th / 1e9 / link,
+            "restore_verify_zero_copy_s": tz, "restore_verify_zero_copy_GB_s": P / tz / 1e9,
+            "snapshot_to_pinned_s": snap_h, "snapshot_to_pinned_GB_s": P / snap_h / 1e9,
+        }
+        del pinned
+
+    if "kv" in rows:
+        result_rows["kv_pool"] = bench_kv(torch, np, gms, synth, timer)
+
+    # ---------------------------------------------------------------- roofline
+    roof = None
+    if main_times:
+        kt = statistics.mean(main_times)
+        alg = 2 * P + 8 * nb  # read image + write entries + read expected hashes
+        achieved = alg / kt / 1e9
+        traffic = None
+        if os.path.exists(TRAFFIC_FILE):
+            with open(TRAFFIC_FILE) as f:
+                tr = json.load(f)
+            if tr.get("kernel_digest") == kernel_source_digest():
+                traffic = tr.get("hbm_bytes_per_launch")
+        roof = {"bound": "hbm", "kernel": "gms::k_stream<restore,hash>", "achieved": round(achieved, 1),
+                "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
+                "traffic": traffic, "algorithmic_bytes_per_launch": alg,
+                "avg_launch_ms": round(kt * 1e3, 4)}
+
+    # ---------------------------------------------------------------- CPU oracle
+    cpu = None
+    if "cpu" in rows:
+        cpu = bench_cpu(torch, np, image, m, specs)
+
+    value = P * args.steps / wall / 1e9 if main_times else None
+    out = {
+        "metric": METRIC,
+        "value": round(value, 2) if value else None,
+        "unit": "GB/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(wall * 1e3 / args.steps, 4) if main_times else None,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "u64",
+        "data": "synthetic (seeded Philox bf16 ~N(0,0.02), generated on the GPU)",
+        "config": {
+            "workload": "llama8b bf16 weight set: 32 layers, d_model 4096, GQA 32q/8kv x 128, SwiGLU ffn 14336, "
+                        "vocab 128256; 291 tensors; device-resident image; fused restore+verify",
+            "payload_bytes": P, "entries": n, "blocks": nb, "chunks": m.num_chunks, "block_bytes": 4096,
+        },
+        "seconds_to_restore_16GB": {
+            "device_image_restore_verify": round(statistics.mean(main_times), 6) if main_times else None,
+            "device_image_plain": round(result_rows["restore_d2d_plain"]["s"], 6) if "restore_d2d_plain" in result_rows else None,
+            "host_pinned_restore_verify": round(result_rows["h2d"]["restore_verify_ring_s"], 4) if "h2d" in result_rows else None,
+        },
+        "roofline": roof,
+        "cpu_baseline": cpu,
+        "rows": result_rows,
+    }
+    print(json.dumps(out), flush=True)
+
+
+def bench_kv(torch, np, gms, synth, timer):
+    """8 GiB paged KV pool: restore only the live blocks + verify, one planted bit flip."""
+    p = synth.kv_pool()
+    pool = [torch.empty(p.layer_bytes, dtype=torch.uint8, device="cuda") for _ in range(p.layers)]
+    for l, t in enumerate(pool):
+        synth.dev_fill_bf16(t.data_ptr(), p.layer_bytes // 2, p.seed, l)
+    live = synth.live_map(p.blocks, p.n_live, p.map_seed, p.map_stream)
+    ents = [(pool[l].data_ptr() + int(b) * p.unit_bytes, p.unit_bytes) for l in range(p.layers) for b in live]
+    m = gms.Manifest(ents, device=0)
+    P, nb = m.payload_bytes, m.num_blocks
+    img = torch.empty(m.image_bytes, dtype=torch.uint8, device="cuda")
+    exp = torch.zeros(nb, dtype=torch.int64, device="cuda")
+    gms.snapshot(m, img, m.image_bytes, blk_hash=exp)
+    # planted corruption: one bit of one live unit in the image
+    e = synth.u64(p.corrupt_seed, p.corrupt_stream, 0) % m.num_entries
+    blk = synth.u64(p.corrupt_seed, p.corrupt_stream, 1) % (p.unit_bytes // 4096)
+    bit = synth.u64(p.corrupt_seed, p.corrupt_stream, 2) % (4096 * 8)
+    off, base = m.layout()
+    byte = off[e] + blk * 4096 + bit // 8
+    img[byte] ^= 1 << (bit % 8)
+    for t in pool:
+        t.fill_(0xA5)
+    cnt = torch.zeros(1, dtype=torch.int64, device="cuda")
+    lst = torch.zeros(8, dtype=torch.int64, device="cuda")
+
+    def run():
+        gms.restore(m, img, m.image_bytes, expected=exp, mismatch_count=cnt, mismatch_list=lst, mismatch_cap=8)
+
+    ts = timer.run(run, 7)
+    c = int(cnt.item())
+    flagged = sorted(int(v) for v in lst[:min(c, 8)].cpu().tolist())
+    # dead units keep the poison
+    dead = np.setdiff1d(np.arange(p.blocks), live)
+    dead_ok = all(bool((t.view(p.blocks, p.unit_bytes)[torch.from_numpy(dead).cuda()] == 0xA5).all()) for t in pool[:4])
+    t = statistics.median(ts)
+    return {"entries": m.num_entries, "payload_bytes": P, "s": t, "GB_s": P / t / 1e9,
+            "hbm_frac": 2 * P / t / 1e9 / HBM_PEAK_GBS, "mismatches": c, "flagged": flagged,
+            "planted_block": int(base[e] + blk), "dead_units_untouched_first4_layers": dead_ok}
+
+
+def bench_cpu(torch, np, image, m, specs):
+    """The CPU oracle, as it stands, on a bounded sample of the same workload."""
+    import oracle
+
+    off, _ = m.layout()
+    k = 1  # the embedding table: 1.05 GB
+    nbytes = [s.nbytes for s in specs[:k]]
+    end = off[k - 1] + -(-nbytes[-1] // 4096) * 4096
+    img = image[:end].cpu().numpy()
+    dst = [np.empty(b, dtype=np.uint8) for b in nbytes]
+    oracle.unpack_into(img, dst)
+    exp, _ = oracle.hashes(dst)
+    reps = []
+    for _ in range(3):
+        t0 = time.perf_counter()
+        oracle.unpack_into(img, dst)
+        c, _ = oracle.verify(dst, exp)
+        reps.append(time.perf_counter() - t0)
+        assert c == 0
+    t = statistics.median(reps)
+    sample = sum(nbytes)
+    return {"value": round(sample / t / 1e9, 4), "unit": "GB/s", "cores": 1, "kind": "oracle",
+            "sample": f"restore+verify (unpack + block-hash compare) of the first {k} tensor(s) of the llama8b "
+                      f"set ({sample} B), single thread, median of 3",
+            "seconds": round(t, 3)}
+
+
+if __name__ == "__main__":
+    main()

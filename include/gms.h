@@ -1,0 +1,205 @@
+/*
+ * libgms: packed device-state image, restore and verify on one AMD Instinct
+ * MI355X (gfx950).
+ *
+ * An engine's GPU-resident state (weight tensors and a fixed pool of mutable
+ * state such as live KV blocks) is described by a manifest of device address
+ * ranges.  gms_snapshot gathers those ranges into one packed image,
+ * gms_restore scatters an image (device-resident or in pinned host memory)
+ * back into the ranges, and gms_verify hashes the live ranges so that
+ * surviving allocations can be checked before they are reattached.
+ *
+ * Where the operations come from (arXiv 2609.25451):
+ *  - Capture stages the engine's remaining device state into host memory and
+ *    recovery reverses the steps, re-creating the allocations
+ *    (section 3.1, Snapshots, capture steps 3-4 and restore).  The data
+ *    transfer part of recovery is about S / B_eff for an artifact of size S
+ *    (section 3.1); the library exists to drive B_eff to the HBM or host-link
+ *    limit, which the paper leaves as future work (section 6, Limitations).
+ *  - The manifest is the recorded tensor layout a GMS client captures before
+ *    commit (section 4, GMS implementation).
+ *  - Verify serves the reattach of surviving allocations by a replacement
+ *    engine (section 3.2, GMS): a schedulable device and the absence of fault
+ *    reports do not show that resident state is intact (section 2.2).
+ *  - Restoring only the live blocks of a fixed private pool follows the
+ *    shadow engine's fixed runtime pool (section 5.3) and KV pages that stay
+ *    reattachable (section 6, Preserving KV state).
+ *
+ * Image layout (the paper fixes none; this is the library's definition):
+ *   entries keep the caller's order; entry i occupies image bytes
+ *   [img_off[i], img_off[i] + roundup(n_i, 4096)), img_off[0] = 0,
+ *   img_off[i+1] = img_off[i] + roundup(n_i, 4096); bytes past n_i in that
+ *   slot are zero after a snapshot.  There is no in-band header: the manifest
+ *   and the hashes travel beside the image.
+ *
+ * Hash (the paper fixes none; this is the library's definition):
+ *   all integers little-endian, arithmetic mod 2^64,
+ *   G = 0x9E3779B97F4A7C15, mix(z) = splitmix64's output function
+ *   (z ^= z>>30; z *= 0xBF58476D1CE4E5B9; z ^= z>>27; z *= 0x94D049BB133111EB;
+ *   z ^= z>>31).  W_i[j] = bytes 8j..8j+7 of entry i, bytes past n_i read as 0,
+ *   j < ceil(n_i/8) the entry-relative word index.
+ *   Block hash Hb(i,b) = XOR of mix(W_i[j] ^ j*G) over the words of 4 KiB block
+ *   b (the last block only its real words); it is stored at global block index
+ *   blk_base[i] + b, blk_base[i] = img_off[i] / 4096.
+ *   Tensor hash Ht(i) = XOR_b Hb(i,b); an empty entry hashes to 0.
+ *   mix is a bijection, so any change confined to one 8-byte word changes that
+ *   block's hash.
+ *
+ * Conventions for every data-plane call (gms_snapshot, gms_restore,
+ * gms_verify):
+ *  - Asynchronous on `stream` (a hipStream_t passed as void*, NULL = the
+ *    device's null stream); outputs are valid once the stream has drained.
+ *    The call returns after enqueueing; argument errors are reported before
+ *    anything is enqueued.
+ *  - Device pointers must be hipMalloc'd memory of the manifest's device
+ *    (sub-ranges of a caching allocator's blocks are fine); the library checks
+ *    every range against its allocation and returns GMS_ERR_INVALID if it
+ *    falls outside one.  The image base must be 16-byte aligned.
+ *  - Hash/mismatch arrays are uint64_t device arrays: blk_hash has
+ *    gms_num_blocks() entries, ten_hash gms_num_entries(), mismatch_count one,
+ *    mismatch_list `mismatch_cap`.  Every output pointer may be NULL unless
+ *    stated otherwise; with all of them NULL the call is a plain copy.
+ *  - A verify mismatch is not an error: the call returns GMS_OK and the count
+ *    is > 0.  The mismatch list holds min(count, cap) global block indices in
+ *    an unspecified order (sort it for a unique result).
+ *  - Calls on one manifest that use the pinned-host staging ring are ordered
+ *    by the library; other calls that write the same memory from different
+ *    streams race, as any two kernels would.
+ *  - No exception, abort or hipMalloc failure crosses the ABI: each call
+ *    returns a status; gms_last_error() gives the calling thread's last
+ *    message.
+ */
+#ifndef GMS_H
+#define GMS_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define GMS_BLOCK_BYTES 4096u
+#define GMS_DEFAULT_CHUNK_BYTES (256u * 1024u)
+#define GMS_HOST_ONLY (-1)
+
+/* One device address range of engine state: [addr, addr + nbytes). */
+typedef struct gms_entry {
+    uint64_t addr;
+    uint64_t nbytes;
+} gms_entry;
+
+/* Opaque; owns the layout, the device-side work list and the staging ring. */
+typedef struct gms_manifest gms_manifest;
+
+enum gms_status {
+    GMS_OK = 0,
+    GMS_ERR_INVALID = -1, /* bad pointer, size, alignment, kind or device  */
+    GMS_ERR_OVERLAP = -2, /* two non-empty entries share bytes             */
+    GMS_ERR_SIZE = -3,    /* image (or output array) smaller than required */
+    GMS_ERR_HIP = -4,     /* a HIP runtime call failed (see last error)     */
+    GMS_ERR_NOMEM = -5,   /* host or device allocation failed              */
+    GMS_ERR_STATE = -6    /* data-plane call on a host-only manifest       */
+};
+
+enum gms_mem_kind {
+    GMS_MEM_DEVICE = 0,      /* image is device memory of the manifest's GPU       */
+    GMS_MEM_HOST_PINNED = 1  /* image is pinned host memory (hipHostMalloc / torch
+                                pin_memory), moved through the staging ring       */
+};
+
+/*
+ * Build a manifest over `n` entries (caller order is the image order).
+ *  entries      host array of n ranges; zero-length entries are allowed and
+ *               occupy no image bytes.
+ *  device       HIP device ordinal that owns every range, or GMS_HOST_ONLY for
+ *               a manifest that only answers layout queries (no HIP call is
+ *               made; data-plane calls return GMS_ERR_STATE).
+ *  chunk_bytes  work-item size: entries are cut at image offsets that are
+ *               multiples of it; 0 selects GMS_DEFAULT_CHUNK_BYTES; otherwise a
+ *               multiple of 4096 in [4096, 64 MiB].
+ *  out          receives the manifest (caller frees with gms_manifest_destroy).
+ * Errors: GMS_ERR_INVALID (NULL pointers, n >= 2^32, address overflow, a range
+ * that is not inside one allocation of `device`), GMS_ERR_OVERLAP, GMS_ERR_NOMEM,
+ * GMS_ERR_HIP.  Synchronous (uploads the work list).
+ */
+int gms_manifest_create(const gms_entry *entries, uint64_t n, int device, uint64_t chunk_bytes,
+                        gms_manifest **out);
+
+/* Frees the manifest and its device work list / staging ring.  NULL is a no-op.
+ * The caller must have drained every stream that still uses the manifest. */
+void gms_manifest_destroy(gms_manifest *m);
+
+/* Layout queries (valid for host-only manifests too; 0 for NULL). */
+uint64_t gms_num_entries(const gms_manifest *m);
+uint64_t gms_payload_bytes(const gms_manifest *m); /* sum of n_i                 */
+uint64_t gms_image_bytes(const gms_manifest *m);   /* sum of roundup(n_i, 4096)  */
+uint64_t gms_num_blocks(const gms_manifest *m);    /* sum of ceil(n_i / 4096)    */
+uint64_t gms_num_chunks(const gms_manifest *m);    /* work items                 */
+int gms_manifest_device(const gms_manifest *m);
+
+/* Copies img_off[n] and blk_base[n] (host arrays; either may be NULL). */
+int gms_layout(const gms_manifest *m, uint64_t *img_off, uint64_t *blk_base);
+
+/*
+ * Staging ring for pinned-host images: `slots` device buffers of `slice_bytes`
+ * (rounded down to a multiple of the chunk size, at least one chunk).  Host
+ * slices are DMA'd into free slots on a library-owned copy stream while the
+ * scatter/gather kernels drain filled slots on the caller's stream.
+ * slots == 0 selects zero-copy: the kernels read/write the pinned image
+ * directly over the host link.  Defaults: 64 MiB x 4.  Takes effect at the next
+ * pinned-host call; frees the old ring after draining it.  Synchronous.
+ */
+int gms_manifest_set_staging(gms_manifest *m, uint64_t slice_bytes, uint32_t slots);
+
+/*
+ * Snapshot (gather): image[img_off[i] + k] = entry_i[k] for k < n_i, zero in
+ * the rest of each slot.  Optionally emits the block / tensor hashes of the
+ * gathered bytes in the same pass (the expected hashes for later checks).
+ *  image, image_bytes, image_kind  destination image (>= gms_image_bytes).
+ *  blk_hash_out, ten_hash_out      optional device outputs.
+ * Errors: GMS_ERR_STATE, GMS_ERR_INVALID, GMS_ERR_SIZE, GMS_ERR_HIP, GMS_ERR_NOMEM.
+ */
+int gms_snapshot(const gms_manifest *m, void *image, uint64_t image_bytes, int image_kind,
+                 uint64_t *blk_hash_out, uint64_t *ten_hash_out, void *stream);
+
+/*
+ * Restore (scatter): entry_i[k] = image[img_off[i] + k] for k < n_i.  No other
+ * byte of any allocation is written.  With hashing requested the words are
+ * hashed in registers as they are stored (no extra HBM traffic): the block
+ * hashes of the restored bytes go to blk_hash_out, the tensor hashes to
+ * ten_hash_out, and if expected_blk is given each block is compared with it;
+ * mismatching global block indices are counted in *mismatch_count_out
+ * (required when expected_blk is set; zeroed by the call) and the first
+ * mismatch_cap of them written to mismatch_list_out.
+ * Errors: as gms_snapshot.
+ */
+int gms_restore(const gms_manifest *m, const void *image, uint64_t image_bytes, int image_kind,
+                const uint64_t *expected_blk, uint64_t *blk_hash_out, uint64_t *ten_hash_out,
+                uint64_t *mismatch_count_out, uint64_t *mismatch_list_out, uint64_t mismatch_cap,
+                void *stream);
+
+/*
+ * Verify (read-only): hashes the live entries in place.  Outputs as
+ * gms_restore; at least one of blk_hash_out, ten_hash_out, expected_blk must be
+ * given.  Verifying an image needs no separate call: a manifest whose entries
+ * are image + img_off[i] with the same sizes hashes identically.
+ * Errors: GMS_ERR_STATE, GMS_ERR_INVALID, GMS_ERR_HIP.
+ */
+int gms_verify(const gms_manifest *m, const uint64_t *expected_blk, uint64_t *blk_hash_out,
+               uint64_t *ten_hash_out, uint64_t *mismatch_count_out, uint64_t *mismatch_list_out,
+               uint64_t mismatch_cap, void *stream);
+
+/* Static description of a status code. */
+const char *gms_status_str(int status);
+
+/* The calling thread's last error message ("" if none); valid until its next call. */
+const char *gms_last_error(void);
+
+/* ABI version of this header (1). */
+int gms_abi_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* GMS_H */

@@ -1,0 +1,220 @@
+"""Python binding of libgms (include/gms.h): argument marshalling only.
+
+Every step of snapshot / restore / verify runs in the HIP library
+``libgms.so`` built next to this file; importing this package fails loudly if
+it is missing.  Pointers may be given as integers or as objects with a
+``data_ptr()`` method (torch tensors); streams as integers or objects with a
+``cuda_stream`` attribute (torch streams), defaulting to torch's current
+stream when torch is importable.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import re
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libgms.so")
+HEADER_PATH = os.path.join(os.path.dirname(_HERE), "include", "gms.h")
+
+try:  # load torch's HIP runtime first so that the library and torch share one runtime
+    import torch  # noqa: F401
+except ImportError:  # plain C-pointer use without torch
+    torch = None
+
+if not os.path.exists(LIB_PATH):
+    raise ImportError(f"{LIB_PATH} is not built; run __graft_entry__.build() (no fallback exists)")
+
+_lib = ctypes.CDLL(LIB_PATH)
+
+U64 = ctypes.c_uint64
+VP = ctypes.c_void_p
+INT = ctypes.c_int
+
+GMS_OK = 0
+GMS_ERR_INVALID = -1
+GMS_ERR_OVERLAP = -2
+GMS_ERR_SIZE = -3
+GMS_ERR_HIP = -4
+GMS_ERR_NOMEM = -5
+GMS_ERR_STATE = -6
+MEM_DEVICE = 0
+MEM_HOST_PINNED = 1
+HOST_ONLY = -1
+BLOCK_BYTES = 4096
+
+
+class GmsEntry(ctypes.Structure):
+    _fields_ = [("addr", U64), ("nbytes", U64)]
+
+
+def _sig(name, res, args):
+    f = getattr(_lib, name)
+    f.restype = res
+    f.argtypes = args
+    return f
+
+
+_create = _sig("gms_manifest_create", INT, [ctypes.POINTER(GmsEntry), U64, INT, U64, ctypes.POINTER(VP)])
+_destroy = _sig("gms_manifest_destroy", None, [VP])
+_num_entries = _sig("gms_num_entries", U64, [VP])
+_payload = _sig("gms_payload_bytes", U64, [VP])
+_image_bytes = _sig("gms_image_bytes", U64, [VP])
+_num_blocks = _sig("gms_num_blocks", U64, [VP])
+_num_chunks = _sig("gms_num_chunks", U64, [VP])
+_device = _sig("gms_manifest_device", INT, [VP])
+_layout = _sig("gms_layout", INT, [VP, VP, VP])
+_set_staging = _sig("gms_manifest_set_staging", INT, [VP, U64, ctypes.c_uint32])
+_snapshot = _sig("gms_snapshot", INT, [VP, VP, U64, INT, VP, VP, VP])
+_restore = _sig("gms_restore", INT, [VP, VP, U64, INT, VP, VP, VP, VP, VP, U64, VP])
+_verify = _sig("gms_verify", INT, [VP, VP, VP, VP, VP, VP, U64, VP])
+_status_str = _sig("gms_status_str", ctypes.c_char_p, [INT])
+_last_error = _sig("gms_last_error", ctypes.c_char_p, [])
+_abi = _sig("gms_abi_version", INT, [])
+
+
+class GmsError(RuntimeError):
+    def __init__(self, status: int, call: str):
+        self.status = status
+        msg = _last_error().decode(errors="replace")
+        super().__init__(f"{call}: {_status_str(status).decode()} ({status}): {msg}")
+
+
+def _check(rc: int, call: str) -> None:
+    if rc != GMS_OK:
+        raise GmsError(rc, call)
+
+
+def _ptr(x) -> int | None:
+    if x is None:
+        return None
+    if hasattr(x, "data_ptr"):
+        return int(x.data_ptr())
+    return int(x)
+
+
+def _stream(stream) -> int | None:
+    if stream is None:
+        if torch is not None and torch.cuda.is_available():
+            return int(torch.cuda.current_stream().cuda_stream) or None
+        return None
+    return int(getattr(stream, "cuda_stream", stream)) or None
+
+
+def abi_version() -> int:
+    return int(_abi())
+
+
+def exported_symbols_declared() -> list[str]:
+    """Names of the functions include/gms.h declares."""
+    with open(HEADER_PATH) as f:
+        text = f.read()
+    return sorted(set(re.findall(r"\b(gms_[a-z_0-9]+)\s*\(", text)))
+
+
+class Manifest:
+    """A manifest over device ranges ``entries`` = [(addr, nbytes)] or tensors."""
+
+    def __init__(self, entries, device: int = 0, chunk_bytes: int = 0):
+        ranges = []
+        for e in entries:
+            if hasattr(e, "data_ptr"):
+                ranges.append((int(e.data_ptr()), int(e.numel() * e.element_size())))
+            else:
+                ranges.append((int(e[0]), int(e[1])))
+        n = len(ranges)
+        arr = (GmsEntry * max(n, 1))(*[GmsEntry(a, b) for a, b in ranges])
+        h = VP()
+        _check(_create(arr, n, device, chunk_bytes, ctypes.byref(h)), "gms_manifest_create")
+        self._h = h
+        self.sizes = [b for _, b in ranges]
+
+    @property
+    def handle(self) -> int:
+        return self._h.value
+
+    def close(self) -> None:
+        if getattr(self, "_h", None) is not None and self._h.value:
+            _destroy(self._h)
+            self._h = VP()
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    def __enter__(self):
+        return self
+
+    def __exit__(self, *exc):
+        self.close()
+
+    @property
+    def num_entries(self) -> int:
+        return int(_num_entries(self._h))
+
+    @property
+    def payload_bytes(self) -> int:
+        return int(_payload(self._h))
+
+    @property
+    def image_bytes(self) -> int:
+        return int(_image_bytes(self._h))
+
+    @property
+    def num_blocks(self) -> int:
+        return int(_num_blocks(self._h))
+
+    @property
+    def num_chunks(self) -> int:
+        return int(_num_chunks(self._h))
+
+    @property
+    def device(self) -> int:
+        return int(_device(self._h))
+
+    def layout(self):
+        """(img_off, blk_base) as lists of ints."""
+        n = self.num_entries
+        off = (U64 * max(n, 1))()
+        base = (U64 * max(n, 1))()
+        _check(_layout(self._h, off, base), "gms_layout")
+        return list(off[:n]), list(base[:n])
+
+    def set_staging(self, slice_bytes: int, slots: int) -> None:
+        _check(_set_staging(self._h, slice_bytes, slots), "gms_manifest_set_staging")
+
+
+def snapshot(m: Manifest, image, image_bytes: int, kind: int = MEM_DEVICE, blk_hash=None, ten_hash=None,
+             stream=None) -> None:
+    _check(_snapshot(m._h, _ptr(image), image_bytes, kind, _ptr(blk_hash), _ptr(ten_hash), _stream(stream)),
+           "gms_snapshot")
+
+
+def restore(m: Manifest, image, image_bytes: int, kind: int = MEM_DEVICE, expected=None, blk_hash=None,
+            ten_hash=None, mismatch_count=None, mismatch_list=None, mismatch_cap: int = 0, stream=None) -> None:
+    _check(_restore(m._h, _ptr(image), image_bytes, kind, _ptr(expected), _ptr(blk_hash), _ptr(ten_hash),
+                    _ptr(mismatch_count), _ptr(mismatch_list), mismatch_cap, _stream(stream)), "gms_restore")
+
+
+def verify(m: Manifest, expected=None, blk_hash=None, ten_hash=None, mismatch_count=None, mismatch_list=None,
+           mismatch_cap: int = 0, stream=None) -> None:
+    _check(_verify(m._h, _ptr(expected), _ptr(blk_hash), _ptr(ten_hash), _ptr(mismatch_count),
+                   _ptr(mismatch_list), mismatch_cap, _stream(stream)), "gms_verify")
+
+
+def status_str(rc: int) -> str:
+    return _status_str(rc).decode()
+
+
+# raw entry points, same names as the C-ABI, for callers that manage pointers themselves
+gms_manifest_create = _create
+gms_manifest_destroy = _destroy
+gms_snapshot = _snapshot
+gms_restore = _restore
+gms_verify = _verify
+gms_layout = _layout
+gms_manifest_set_staging = _set_staging
+gms_status_str = _status_str
+gms_last_error = _last_error

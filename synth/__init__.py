@@ -51,6 +51,7 @@ def _load_host():
 def _load_dev():
     global _dev
     if _dev is None:
+        import torch  # noqa: F401  (load torch's HIP runtime before the generator's)
         path = os.path.join(_HERE, "libsynth_dev.so")
         if not os.path.exists(path):
             raise RuntimeError(f"{path} is not built; run __graft_entry__.build()")

@@ -1,0 +1,127 @@
+"""C-ABI surface on the CPU: symbols, layout queries, argument validation.
+
+Host-only manifests (device = -1) exercise every host-side rule without a GPU;
+no data-plane call here reaches a kernel.
+"""
+import ctypes
+import subprocess
+
+import numpy as np
+import pytest
+
+import oracle
+import paper_2609_25451_amd as gms
+import synth
+
+
+def test_exports_every_declared_symbol():
+    declared = gms.exported_symbols_declared()
+    assert "gms_restore" in declared and "gms_manifest_create" in declared
+    out = subprocess.run(["nm", "-D", "--defined-only", gms.LIB_PATH], capture_output=True, text=True,
+                         check=True).stdout
+    exported = {line.split()[-1] for line in out.splitlines() if line.strip()}
+    missing = [s for s in declared if s not in exported]
+    assert not missing, f"declared but not exported: {missing}"
+    assert gms.abi_version() == 1
+
+
+def _host_manifest(sizes, base=1 << 40, gap=0, chunk_bytes=0):
+    ents, a = [], base
+    for s in sizes:
+        ents.append((a, s))
+        a += s + gap
+    return gms.Manifest(ents, device=gms.HOST_ONLY, chunk_bytes=chunk_bytes)
+
+
+def test_layout_matches_oracle():
+    rng = np.random.default_rng(1)
+    for _ in range(30):
+        sizes = [int(v) for v in rng.integers(0, 50_000, rng.integers(0, 40))]
+        m = _host_manifest(sizes, gap=int(rng.integers(0, 9)))
+        off, base = m.layout()
+        o_off, o_base, o_ib, o_nb = oracle.layout(sizes)
+        assert off == [int(v) for v in o_off] and base == [int(v) for v in o_base]
+        assert m.image_bytes == o_ib and m.num_blocks == o_nb and m.payload_bytes == sum(sizes)
+        assert m.num_entries == len(sizes)
+
+
+def _expected_chunks(sizes, cb):
+    n, off = 0, 0
+    for s in sizes:
+        pos = 0
+        while pos < s:
+            img = off + pos
+            pos += min(s - pos, (img // cb + 1) * cb - img)
+            n += 1
+        off += -(-s // 4096) * 4096
+    return n
+
+
+@pytest.mark.parametrize("name", ["tiny", "llama8b", "llama70b_tp8"])
+def test_workload_layouts(name):
+    _, ts = synth.weight_set(name)
+    sizes = [t.nbytes for t in ts]
+    m = _host_manifest(sizes)
+    _, _, ib, nb = oracle.layout(sizes)
+    assert m.image_bytes == ib and m.num_blocks == nb
+    assert m.num_chunks == _expected_chunks(sizes, 256 * 1024)
+    m4 = _host_manifest(sizes, chunk_bytes=1 << 20)
+    assert m4.num_chunks == _expected_chunks(sizes, 1 << 20)
+
+
+def test_kv_pool_layout():
+    p = synth.kv_pool()
+    live = synth.live_map(p.blocks, p.n_live, p.map_seed, p.map_stream)
+    ents = [((1 << 40) + l * p.layer_bytes + int(b) * p.unit_bytes, p.unit_bytes)
+            for l in range(p.layers) for b in live]
+    m = gms.Manifest(ents, device=gms.HOST_ONLY)
+    assert m.num_entries == 78_624 and m.payload_bytes == 5_152_702_464 == m.image_bytes
+    assert m.num_blocks == 78_624 * 16 and m.num_chunks == 78_624
+
+
+def test_overlap_and_bad_ranges_rejected():
+    with pytest.raises(gms.GmsError) as e:
+        gms.Manifest([(4096, 100), (4096 + 99, 10)], device=gms.HOST_ONLY)
+    assert e.value.status == gms.GMS_ERR_OVERLAP
+    # touching ranges and zero-length entries anywhere are fine
+    m = gms.Manifest([(4096, 100), (4196, 10), (4150, 0), (0, 0)], device=gms.HOST_ONLY)
+    assert m.num_entries == 4 and m.num_blocks == 2
+    for bad in ([(0, 8)], [((1 << 64) - 8, 16)]):
+        with pytest.raises(gms.GmsError) as e:
+            gms.Manifest(bad, device=gms.HOST_ONLY)
+        assert e.value.status == gms.GMS_ERR_INVALID
+    for cb in (1000, 4096 * 3 + 1, 128 << 20):
+        with pytest.raises(gms.GmsError) as e:
+            gms.Manifest([(4096, 10)], device=gms.HOST_ONLY, chunk_bytes=cb)
+        assert e.value.status == gms.GMS_ERR_INVALID
+
+
+def test_empty_manifest():
+    m = gms.Manifest([], device=gms.HOST_ONLY)
+    assert m.num_entries == 0 and m.image_bytes == 0 and m.num_blocks == 0 and m.num_chunks == 0
+    assert m.layout() == ([], [])
+
+
+def test_data_plane_refused_on_host_only_manifest():
+    m = _host_manifest([5000, 3])
+    for call in (lambda: gms.snapshot(m, 1 << 30, m.image_bytes, stream=0),
+                 lambda: gms.restore(m, 1 << 30, m.image_bytes, stream=0),
+                 lambda: gms.verify(m, blk_hash=1 << 30, stream=0)):
+        with pytest.raises(gms.GmsError) as e:
+            call()
+        assert e.value.status == gms.GMS_ERR_STATE
+    with pytest.raises(gms.GmsError) as e:
+        m.set_staging(1 << 20, 2)
+    assert e.value.status == gms.GMS_ERR_STATE
+
+
+def test_null_arguments():
+    out = ctypes.c_void_p()
+    assert gms.gms_manifest_create(None, 3, gms.HOST_ONLY, 0, ctypes.byref(out)) == gms.GMS_ERR_INVALID
+    assert gms.gms_manifest_create(None, 0, gms.HOST_ONLY, 0, None) == gms.GMS_ERR_INVALID
+    assert gms.gms_snapshot(None, None, 0, 0, None, None, None) == gms.GMS_ERR_INVALID
+    assert gms.gms_restore(None, None, 0, 0, None, None, None, None, None, 0, None) == gms.GMS_ERR_INVALID
+    assert gms.gms_verify(None, None, None, None, None, None, 0, None) == gms.GMS_ERR_INVALID
+    assert b"null" in gms.gms_last_error()
+    for rc in (0, -1, -2, -3, -4, -5, -6, 7):
+        assert gms.status_str(rc)

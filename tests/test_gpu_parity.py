@@ -1,0 +1,276 @@
+"""GPU path vs the CPU oracle, element by element, at sizes the oracle finishes quickly.
+
+Every case: snapshot image == oracle pack; restored bytes == source with every
+byte outside the entries untouched; block / tensor hashes == oracle; mismatch
+lists == oracle verify.  Inputs come from the seeded generator on the host
+(or the GPU generator, itself checked against the host one).
+"""
+import ctypes
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2609_25451_amd as gms
+import synth
+from gpu_util import Arena, from_u64, host_bytes, need_gpu, random_datas, to_u64, u64_dev
+
+pytestmark = pytest.mark.gpu
+
+
+def _image(nbytes, kind, sentinel=0x5A):
+    if kind == gms.MEM_DEVICE:
+        return torch.full((max(nbytes, 16),), sentinel, dtype=torch.uint8, device="cuda")
+    t = torch.empty((max(nbytes, 16),), dtype=torch.uint8, pin_memory=True)
+    t.fill_(sentinel)
+    return t
+
+
+def _round_trip(arena: Arena, datas, kind, chunk_bytes=0, staging=None, check_outside=True):
+    """snapshot -> poison -> fused restore -> verify, all compared with the oracle."""
+    m = gms.Manifest(arena.entries, device=0, chunk_bytes=chunk_bytes)
+    if staging is not None:
+        m.set_staging(*staging)
+    o_img = oracle.pack(datas)
+    o_blk, o_ten = oracle.hashes(datas)
+    nb, n = m.num_blocks, m.num_entries
+    assert m.image_bytes == o_img.nbytes and nb == o_blk.size
+
+    img = _image(m.image_bytes, kind)
+    blk, ten = u64_dev(nb), u64_dev(n)
+    gms.snapshot(m, img, m.image_bytes, kind, blk_hash=blk, ten_hash=ten)
+    torch.cuda.synchronize()
+    got = (img.cpu() if kind == gms.MEM_DEVICE else img).numpy()[: m.image_bytes]
+    assert np.array_equal(got, o_img), "snapshot image differs from the oracle"
+    assert np.array_equal(to_u64(blk, nb), o_blk) and np.array_equal(to_u64(ten, n), o_ten)
+
+    arena.poison()
+    exp = from_u64(o_blk)
+    blk2, ten2, cnt, lst = u64_dev(nb), u64_dev(n), u64_dev(1), u64_dev(8)
+    cnt.fill_(12345)
+    gms.restore(m, img, m.image_bytes, kind, expected=exp, blk_hash=blk2, ten_hash=ten2,
+                mismatch_count=cnt, mismatch_list=lst, mismatch_cap=8)
+    torch.cuda.synchronize()
+    back, whole = arena.read()
+    for i, (a, b) in enumerate(zip(back, datas)):
+        assert np.array_equal(a, b), f"entry {i} restored wrong"
+    if check_outside:
+        assert arena.outside_untouched(whole), "restore wrote outside the manifest"
+    assert to_u64(cnt)[0] == 0
+    assert np.array_equal(to_u64(blk2, nb), o_blk) and np.array_equal(to_u64(ten2, n), o_ten)
+
+    blk3, ten3, cnt3 = u64_dev(nb), u64_dev(n), u64_dev(1)
+    gms.verify(m, expected=exp, blk_hash=blk3, ten_hash=ten3, mismatch_count=cnt3)
+    torch.cuda.synchronize()
+    assert to_u64(cnt3)[0] == 0
+    assert np.array_equal(to_u64(blk3, nb), o_blk) and np.array_equal(to_u64(ten3, n), o_ten)
+    return m, img
+
+
+def test_gpu_generator_matches_host():
+    need_gpu()
+    seed, ts = synth.weight_set("tiny")
+    for t_id in (0, 1, 5, 20):
+        n = ts[t_id].numel
+        d = torch.empty(n, dtype=torch.int16, device="cuda")
+        synth.dev_fill_bf16(d.data_ptr(), n, seed, t_id)
+        torch.cuda.synchronize()
+        assert np.array_equal(d.cpu().numpy().view(np.uint16), synth.bf16_bits(n, seed, t_id))
+    # odd offsets and lengths
+    d = torch.empty(1001, dtype=torch.int16, device="cuda")
+    synth.dev_fill_bf16(d.data_ptr(), 1001, 9, 3, first=77)
+    b = torch.empty(999, dtype=torch.uint8, device="cuda")
+    synth.dev_fill_bytes(b.data_ptr(), 999, 4, 6, first=13)
+    torch.cuda.synchronize()
+    assert np.array_equal(d.cpu().numpy().view(np.uint16), synth.bf16_bits(1001, 9, 3, 77))
+    assert np.array_equal(b.cpu().numpy(), synth.random_bytes(999, 4, 6, 13))
+
+
+@pytest.mark.parametrize("kind", [gms.MEM_DEVICE, gms.MEM_HOST_PINNED])
+def test_tiny_weights_round_trip(kind):
+    need_gpu()
+    seed, ts = synth.weight_set("tiny")
+    tensors = [torch.empty(t.shape, dtype=torch.bfloat16, device="cuda") for t in ts]
+    for i, t in enumerate(tensors):
+        synth.dev_fill_bf16(t.data_ptr(), t.numel(), seed, i)
+    datas = [synth.bf16_bits(t.numel, seed, i).view(np.uint8) for i, t in enumerate(ts)]
+    m = gms.Manifest(tensors, device=0)
+    img = _image(m.image_bytes, kind)
+    blk, ten = u64_dev(m.num_blocks), u64_dev(m.num_entries)
+    gms.snapshot(m, img, m.image_bytes, kind, blk_hash=blk, ten_hash=ten)
+    torch.cuda.synchronize()
+    got = (img.cpu() if kind == gms.MEM_DEVICE else img).numpy()[: m.image_bytes]
+    assert np.array_equal(got, oracle.pack(datas))
+    o_blk, o_ten = oracle.hashes(datas)
+    assert np.array_equal(to_u64(blk), o_blk) and np.array_equal(to_u64(ten), o_ten)
+    for t in tensors:
+        t.view(torch.uint8).fill_(0xA5)
+    cnt = u64_dev(1)
+    gms.restore(m, img, m.image_bytes, kind, expected=from_u64(o_blk), mismatch_count=cnt)
+    torch.cuda.synchronize()
+    assert to_u64(cnt)[0] == 0
+    for t, d in zip(tensors, datas):
+        assert np.array_equal(host_bytes(t), d)
+
+
+RAGGED_SEEDS = list(range(6))
+
+
+@pytest.mark.parametrize("seed", RAGGED_SEEDS)
+@pytest.mark.parametrize("aligned", [True, False])
+def test_ragged_manifest_device(seed, aligned):
+    need_gpu()
+    rng = np.random.default_rng(500 + seed)
+    k = int(rng.integers(1, 40))
+    sizes = [int(v) for v in rng.integers(0, 70_000, k)]
+    sizes[0] = 300_000 + int(rng.integers(0, 5000))  # spans several chunks and a ragged tail
+    if k > 2:
+        sizes[1] = 0
+    arena = Arena(sizes, misalign=None if aligned else (lambda r: r.integers(0, 16)), seed=seed)
+    datas = random_datas(sizes, seed=seed)
+    arena.fill(datas)
+    _round_trip(arena, datas, gms.MEM_DEVICE, chunk_bytes=int(rng.choice([0, 4096, 12288, 1 << 20])))
+
+
+@pytest.mark.parametrize("staging", [None, (256 * 1024, 2), (1 << 20, 3), (0, 0)],
+                         ids=["ring_default", "ring_256k_x2", "ring_1m_x3", "zero_copy"])
+def test_ragged_manifest_pinned(staging):
+    need_gpu()
+    rng = np.random.default_rng(42)
+    sizes = [int(v) for v in rng.integers(0, 200_000, 30)] + [3 << 20, 5, 0, 4096]
+    arena = Arena(sizes, misalign=lambda r: r.integers(0, 16) * int(r.integers(0, 2)), seed=3)
+    datas = random_datas(sizes, seed=11)
+    arena.fill(datas)
+    m, img = _round_trip(arena, datas, gms.MEM_HOST_PINNED, staging=staging)
+    # a second call through the same ring, on another stream
+    arena.poison()
+    s = torch.cuda.Stream()
+    with torch.cuda.stream(s):
+        gms.restore(m, img, m.image_bytes, gms.MEM_HOST_PINNED)
+    s.synchronize()
+    back, whole = arena.read()
+    assert all(np.array_equal(a, b) for a, b in zip(back, datas)) and arena.outside_untouched(whole)
+
+
+def test_plain_copy_without_hashes():
+    need_gpu()
+    sizes = [1 << 20, 4097, 123, 8 << 20]
+    arena = Arena(sizes, misalign=[0, 3, 1, 0])
+    datas = random_datas(sizes, seed=21)
+    arena.fill(datas)
+    m = gms.Manifest(arena.entries, device=0)
+    img = _image(m.image_bytes, gms.MEM_DEVICE)
+    gms.snapshot(m, img, m.image_bytes)
+    arena.poison()
+    gms.restore(m, img, m.image_bytes)
+    torch.cuda.synchronize()
+    assert np.array_equal(img.cpu().numpy()[: m.image_bytes], oracle.pack(datas))
+    back, whole = arena.read()
+    assert all(np.array_equal(a, b) for a, b in zip(back, datas)) and arena.outside_untouched(whole)
+
+
+def test_corruption_flags_exact_blocks():
+    need_gpu()
+    sizes = [5 * 4096, 100, 0, 3 * 4096 + 9, 4096, 700_001]
+    arena = Arena(sizes, misalign=[0, 0, 0, 5, 0, 8])
+    datas = random_datas(sizes, seed=31)
+    arena.fill(datas)
+    m = gms.Manifest(arena.entries, device=0)
+    o_blk, _ = oracle.hashes(datas)
+    exp = from_u64(o_blk)
+    img = _image(m.image_bytes, gms.MEM_DEVICE)
+    gms.snapshot(m, img, m.image_bytes)
+    torch.cuda.synchronize()
+    off, _ = m.layout()
+    rng = np.random.default_rng(8)
+    flips = []
+    for ent in (0, 3, 1, 5, 5):
+        byte = int(rng.integers(0, sizes[ent]))
+        flips.append((ent, byte, int(rng.integers(0, 8))))
+    # flip bits in the image: the fused restore must flag exactly those blocks
+    bad = [d.copy() for d in datas]
+    himg = img.cpu()
+    for ent, byte, bit in flips:
+        himg[off[ent] + byte] ^= 1 << bit
+        bad[ent][byte] ^= np.uint8(1 << bit)
+    img.copy_(himg)
+    want_cnt, want = oracle.verify(bad, o_blk)
+    assert want_cnt >= 4
+    cnt, lst = u64_dev(1), u64_dev(64)
+    gms.restore(m, img, m.image_bytes, expected=exp, mismatch_count=cnt, mismatch_list=lst, mismatch_cap=64)
+    torch.cuda.synchronize()
+    c = int(to_u64(cnt)[0])
+    assert c == want_cnt and np.array_equal(np.sort(to_u64(lst, c)), want)
+    # the restored (corrupted) entries: verify must agree; a small cap truncates
+    cnt2, lst2 = u64_dev(1), u64_dev(2)
+    gms.verify(m, expected=exp, mismatch_count=cnt2, mismatch_list=lst2, mismatch_cap=2)
+    torch.cuda.synchronize()
+    assert int(to_u64(cnt2)[0]) == want_cnt
+    assert set(to_u64(lst2, 2).tolist()) <= set(want.tolist())
+    # the padding of an image slot is not part of any hash
+    himg[off[1] + 200] ^= 0xFF
+    img.copy_(himg)
+    gms.restore(m, img, m.image_bytes, expected=exp, mismatch_count=cnt)
+    torch.cuda.synchronize()
+    assert int(to_u64(cnt)[0]) == want_cnt
+
+
+def test_empty_and_zero_length_manifests():
+    need_gpu()
+    cnt = u64_dev(1)
+    cnt.fill_(99)
+    m = gms.Manifest([], device=0)
+    img = _image(16, gms.MEM_DEVICE)
+    gms.snapshot(m, img, 16)
+    gms.restore(m, img, 16, expected=u64_dev(1), mismatch_count=cnt)
+    torch.cuda.synchronize()
+    assert to_u64(cnt)[0] == 0
+    buf = torch.zeros(64, dtype=torch.uint8, device="cuda")
+    m2 = gms.Manifest([(buf.data_ptr(), 0), (buf.data_ptr() + 8, 0)], device=0)
+    ten = u64_dev(2)
+    ten.fill_(7)
+    gms.verify(m2, ten_hash=ten)
+    torch.cuda.synchronize()
+    assert to_u64(ten, 2).tolist() == [0, 0]
+
+
+def test_argument_errors_on_gpu():
+    need_gpu()
+    buf = torch.zeros(10_000, dtype=torch.uint8, device="cuda")
+    m = gms.Manifest([(buf.data_ptr(), 5000), (buf.data_ptr() + 5000, 3000)], device=0)
+    small = torch.zeros(4096, dtype=torch.uint8, device="cuda")
+    with pytest.raises(gms.GmsError) as e:
+        gms.restore(m, small, small.numel())
+    assert e.value.status == gms.GMS_ERR_SIZE
+    big = torch.zeros(m.image_bytes + 64, dtype=torch.uint8, device="cuda")
+    with pytest.raises(gms.GmsError) as e:
+        gms.restore(m, big.data_ptr() + 1, m.image_bytes)
+    assert e.value.status == gms.GMS_ERR_INVALID
+    host = np.zeros(m.image_bytes, dtype=np.uint8)
+    with pytest.raises(gms.GmsError) as e:
+        gms.restore(m, host.ctypes.data, m.image_bytes, gms.MEM_DEVICE)
+    assert e.value.status == gms.GMS_ERR_INVALID
+    with pytest.raises(gms.GmsError) as e:  # pageable memory is not pinned
+        gms.restore(m, host.ctypes.data, m.image_bytes, gms.MEM_HOST_PINNED)
+    assert e.value.status == gms.GMS_ERR_INVALID
+    # entry running past its allocation (an exact hipMalloc, so the bound is known)
+    hip = ctypes.CDLL("libamdhip64.so.7")
+    raw = ctypes.c_void_p()
+    assert hip.hipMalloc(ctypes.byref(raw), ctypes.c_size_t(1 << 20)) == 0
+    try:
+        with pytest.raises(gms.GmsError) as e:
+            gms.Manifest([(raw.value + (1 << 20) - 100, 4 << 20)], device=0)
+        assert e.value.status == gms.GMS_ERR_SIZE
+        gms.Manifest([(raw.value + 100, (1 << 20) - 100)], device=0).close()
+    finally:
+        hip.hipFree(raw)
+    with pytest.raises(gms.GmsError) as e:  # host memory as an entry
+        gms.Manifest([(host.ctypes.data, 100)], device=0)
+    assert e.value.status == gms.GMS_ERR_INVALID
+    with pytest.raises(gms.GmsError) as e:  # expected without a counter
+        gms.verify(m, expected=u64_dev(m.num_blocks))
+    assert e.value.status == gms.GMS_ERR_INVALID
+    with pytest.raises(gms.GmsError) as e:
+        gms.verify(m)
+    assert e.value.status == gms.GMS_ERR_INVALID
