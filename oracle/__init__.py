@@ -50,6 +50,8 @@ class Oracle:
         lib.oracle_word.restype = U64
         lib.oracle_block_hash.argtypes = [VP, U64, U64]
         lib.oracle_block_hash.restype = U64
+        lib.oracle_block_hash_at.argtypes = [VP, U64, U64]
+        lib.oracle_block_hash_at.restype = U64
         lib.oracle_entry_hashes.argtypes = [VP, U64, VP]
         lib.oracle_entry_hashes.restype = U64
         lib.oracle_layout.argtypes = [VP, U64, VP, VP, VP, VP]
@@ -71,6 +73,13 @@ class Oracle:
     def block_hash(self, x, b: int) -> int:
         x = _u8(x)
         return int(self.lib.oracle_block_hash(x.ctypes.data, x.nbytes, b))
+
+    def block_hash_at(self, blk, n: int, b: int) -> int:
+        """Hash of block b of an n-byte entry, given only that block's bytes."""
+        blk = _u8(blk)
+        if blk.nbytes < min(BLOCK, max(n - BLOCK * b, 0)):
+            raise ValueError("block buffer shorter than the block")
+        return int(self.lib.oracle_block_hash_at(blk.ctypes.data, n, b))
 
     def entry_hashes(self, x):
         """(block hashes [ceil(n/4096)] uint64, tensor hash int) of one entry."""
@@ -159,6 +168,10 @@ def word(x, j):
 
 def block_hash(x, b):
     return default().block_hash(x, b)
+
+
+def block_hash_at(blk, n, b):
+    return default().block_hash_at(blk, n, b)
 
 
 def entry_hashes(x):

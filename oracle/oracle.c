@@ -51,16 +51,35 @@ uint64_t oracle_word(const uint8_t *x, uint64_t n, uint64_t j)
 
 static uint64_t ceil_div(uint64_t a, uint64_t b) { return a / b + (a % b != 0); }
 
+/* Hb of a block whose `len` (<= 4096) real bytes start at blk and whose first
+ * word has entry-relative index j0. */
+static uint64_t hash_block_bytes(const uint8_t *blk, uint64_t len, uint64_t j0)
+{
+    uint64_t h = 0;
+    for (uint64_t q = 0; q < ceil_div(len, 8); ++q)
+        h ^= oracle_fmix(oracle_word(blk, len, q) ^ ((j0 + q) * ORACLE_G));
+    return h;
+}
+
+/* Real bytes of block b of an n-byte entry (0 past the last block). */
+static uint64_t block_len(uint64_t n, uint64_t b)
+{
+    uint64_t lo = ORACLE_BLOCK * b;
+    if (lo >= n) return 0;
+    return n - lo < ORACLE_BLOCK ? n - lo : ORACLE_BLOCK;
+}
+
 uint64_t oracle_block_hash(const uint8_t *x, uint64_t n, uint64_t b)
 {
-    const uint64_t words_per_block = ORACLE_BLOCK / 8;
-    uint64_t nwords = ceil_div(n, 8);
-    uint64_t j_end = words_per_block * (b + 1);
-    if (j_end > nwords) j_end = nwords;
-    uint64_t h = 0;
-    for (uint64_t j = words_per_block * b; j < j_end; ++j)
-        h ^= oracle_fmix(oracle_word(x, n, j) ^ (j * ORACLE_G));
-    return h;
+    uint64_t len = block_len(n, b);
+    return len ? hash_block_bytes(x + ORACLE_BLOCK * b, len, ORACLE_BLOCK * b / 8) : 0;
+}
+
+/* Same as oracle_block_hash, given only block b's bytes (blk) of an n-byte entry. */
+uint64_t oracle_block_hash_at(const uint8_t *blk, uint64_t n, uint64_t b)
+{
+    uint64_t len = block_len(n, b);
+    return len ? hash_block_bytes(blk, len, ORACLE_BLOCK * b / 8) : 0;
 }
 
 /* Writes ceil(n/4096) block hashes (if blk_out) and returns the tensor hash. */

@@ -33,6 +33,7 @@
 uint64_t oracle_fmix(uint64_t z);
 uint64_t oracle_word(const uint8_t *x, uint64_t n, uint64_t j);
 uint64_t oracle_block_hash(const uint8_t *x, uint64_t n, uint64_t b);
+uint64_t oracle_block_hash_at(const uint8_t *blk, uint64_t n, uint64_t b);
 uint64_t oracle_entry_hashes(const uint8_t *x, uint64_t n, uint64_t *blk_out);
 void oracle_layout(const uint64_t *nbytes, uint64_t count, uint64_t *img_off, uint64_t *blk_base,
                    uint64_t *image_bytes, uint64_t *num_blocks);

@@ -181,6 +181,16 @@ def pin_entry_relative_and_xor(o):
     assert acc == ta, "tensor hash is the XOR of its block hashes, in any order"
 
 
+def pin_block_hash_at(o):
+    """The by-position block hash agrees with the whole-entry one, including ragged tails."""
+    rng = np.random.default_rng(19)
+    for n in [1, 8, 4095, 4096, 4097, 3 * BLOCK + 123, 5 * BLOCK]:
+        x = rng.integers(0, 256, n, dtype=np.uint8)
+        for b in range(-(-n // BLOCK)):
+            assert o.block_hash_at(x[BLOCK * b: BLOCK * (b + 1)].copy(), n, b) == o.block_hash(x, b)
+        assert o.block_hash(x, -(-n // BLOCK)) == 0
+
+
 def pin_layout(o):
     rng = np.random.default_rng(13)
     for _ in range(50):
@@ -287,6 +297,7 @@ ALL_PINS = [
     pin_zero_blocks_closed_form,
     pin_swaps_and_positions,
     pin_entry_relative_and_xor,
+    pin_block_hash_at,
     pin_layout,
     pin_roundtrip,
     pin_verify,

@@ -20,13 +20,16 @@ MUTANTS = [
     ("c2_digit", "0x94D049BB133111EBull", "0x94D049BB133111EDull"),
     ("g_digit", "0x9E3779B97F4A7C15ull", "0x9E3779B97F4A7C17ull"),
     ("drop_last_xorshift", "    z ^= z >> 31;\n", ""),
-    ("index_block_relative", "(j * ORACLE_G)", "((j % words_per_block) * ORACLE_G)"),
-    ("index_dropped", "oracle_word(x, n, j) ^ (j * ORACLE_G)", "oracle_word(x, n, j)"),
-    ("index_plus_one", "(j * ORACLE_G)", "((j + 1) * ORACLE_G)"),
+    ("index_block_relative", "((j0 + q) * ORACLE_G)", "(q * ORACLE_G)"),
+    ("index_dropped", "oracle_word(blk, len, q) ^ ((j0 + q) * ORACLE_G)", "oracle_word(blk, len, q)"),
+    ("index_plus_one", "((j0 + q) * ORACLE_G)", "((j0 + q + 1) * ORACLE_G)"),
+    ("index_bytes_not_words", "ORACLE_BLOCK * b / 8) : 0;\n}\n\n/* Same", "ORACLE_BLOCK * b) : 0;\n}\n\n/* Same"),
     ("big_endian_word", "w |= byte << (8 * k);", "w |= byte << (8 * (7 - k));"),
     ("pad_with_ones", "pos < n ? x[pos] : 0;", "pos < n ? x[pos] : 0xFF;"),
-    ("hash_pad_words", "    if (j_end > nwords) j_end = nwords;\n", "    if (j_end > nwords + 1) j_end = nwords + 1;\n"),
-    ("block_of_1024_words", "const uint64_t words_per_block = ORACLE_BLOCK / 8;", "const uint64_t words_per_block = ORACLE_BLOCK / 4;"),
+    ("hash_pad_words", "q < ceil_div(len, 8); ++q", "q < ceil_div(len, 8) + (len < ORACLE_BLOCK); ++q"),
+    ("block_8k", '#include "oracle.h"\n', '#include "oracle.h"\n#undef ORACLE_BLOCK\n#define ORACLE_BLOCK 8192u\n'),
+    ("last_word_truncated", "return n - lo < ORACLE_BLOCK ? n - lo : ORACLE_BLOCK;",
+     "return n - lo < ORACLE_BLOCK ? (n - lo) / 8 * 8 : ORACLE_BLOCK;"),
     ("tensor_add", "        t ^= hb;", "        t += hb;"),
     ("layout_unaligned", "        off += ceil_div(nbytes[i], ORACLE_BLOCK) * ORACLE_BLOCK;\n        blk +=",
      "        off += nbytes[i];\n        blk +="),
