@@ -8,7 +8,7 @@
 namespace gms {
 
 constexpr uint32_t kBlockBytes = 4096;  // hash block and image alignment
-constexpr int kThreads = 256;           // 4 wave64s per workgroup
+constexpr int kThreads = 512;           // 8 wave64s per workgroup
 
 // One workgroup's unit of work: a piece of one entry that never crosses an
 // image offset that is a multiple of the manifest's chunk size.

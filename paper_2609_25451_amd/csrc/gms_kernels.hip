@@ -1,18 +1,25 @@
 // Gather / scatter / verify kernels for gfx950.
 //
-// One workgroup (4 wave64s) takes one chunk of the manifest's work list; each
-// wave walks the chunk's 4 KiB blocks with stride 4.  For one block a lane
+// One workgroup (8 wave64s) takes one chunk of the manifest's work list; each
+// wave walks the chunk's 4 KiB blocks with stride 8.  For one block a lane
 // moves four 16-byte segments at byte offsets k*1024 + lane*16 (k = 0..3), so
 // every load and store instruction of the wave covers 1 KiB contiguously.
+// Each wave keeps the loads of its next two blocks in flight while it stores
+// and hashes the current one, and restore/snapshot launches reserve enough
+// LDS to hold residency at one workgroup per CU: on MI355X a copy reaches its
+// best HBM efficiency with about eight deep streams per CU rather than many
+// shallow ones (pure reads run at ~90% of peak, pure writes at ~72%).
 // Hashing happens on the registers that were just moved: each lane mixes its
 // eight 8-byte words, the wave XOR-reduces its 64 partials with DPP row
 // operations plus four lane reads, and lane 0 stores / compares the block
-// hash.  Tensor hashes combine the four waves' XORs in LDS and take one 64-bit
-// atomic XOR per chunk.
+// hash.  Tensor hashes combine the eight waves' XORs in LDS and take one
+// 64-bit atomic XOR per chunk.
 //
 // Bandwidth path: no MFMA; 16-byte non-temporal loads and stores for the
 // streaming side; byte-granular code only for unaligned entries and the ragged
 // last block of an entry.
+
+#include <mutex>
 
 #include "gms_internal.h"
 
@@ -29,6 +36,9 @@ constexpr uint64_t kG = 0x9E3779B97F4A7C15ull;   // index multiplier
 constexpr uint64_t kMulA = 0xBF58476D1CE4E5B9ull;
 constexpr uint64_t kMulB = 0x94D049BB133111EBull;
 constexpr uint64_t kSegStrideG = 128ull * kG;    // word-index step between a lane's segments
+constexpr uint64_t kBlockStrideG = 512ull * kG;  // word-index step between blocks
+constexpr int kWaves = kThreads / 64;            // waves per workgroup
+constexpr int kDepth = 2;                        // blocks each wave keeps loading ahead
 
 __device__ __forceinline__ uint64_t mix64(uint64_t z)
 {
@@ -121,94 +131,158 @@ __device__ __forceinline__ void store_part(gbyte *p, u32x4 v, uint32_t valid, bo
         p[q] = (uint8_t)(q < 8 ? (w0 >> (8 * q)) : (w1 >> (8 * (q - 8))));
 }
 
+// Block epilogue.  `hl` is the lane's partial hash; with `check` set, lane 0
+// folds the expected hash `want` into the reduction, so the reduced value is
+// zero exactly when the block matches and `want` never has to leave its vector
+// register.  Lane 0 stores the block hash / records a mismatch.  Returns the
+// block hash in a vector register (meaningful in lane 0).
+__device__ __forceinline__ uint64_t finish_block(uint64_t hl, uint64_t gblk, const HashOut &h, uint32_t lane,
+                                                 bool check, uint64_t want)
+{
+    const uint64_t fold = (check && lane == 0) ? want : 0;
+    const uint64_t red = wave_xor64(hl ^ fold);  // block hash, XOR want when checking
+    const uint64_t hb = red ^ fold;
+    if (lane == 0) {
+        if (h.blk) h.blk[gblk] = hb;
+        if (check && red != 0) {
+            const uint64_t at = atomicAdd((unsigned long long *)h.mm_count, 1ull);
+            if (h.mm_list && at < h.mm_cap) h.mm_list[at] = gblk;
+        }
+    }
+    return hb;
+}
+
+// The lane's four 16-byte segments of the full 4 KiB block at p.
+__device__ __forceinline__ void load_block(u32x4 v[4], const gbyte *p)
+{
+#pragma unroll
+    for (int k = 0; k < 4; ++k) v[k] = __builtin_nontemporal_load((const gvec *)(p + k * 1024));
+}
+
+__device__ __forceinline__ void store_block(const u32x4 v[4], gbyte *p)
+{
+#pragma unroll
+    for (int k = 0; k < 4; ++k) __builtin_nontemporal_store(v[k], (gvec *)(p + k * 1024));
+}
+
+__device__ __forceinline__ uint32_t fast_blocks(const Chunk &c)
+{
+    return (c.addr & 15) == 0 ? c.len / kBlockBytes : 0;
+}
+
+// One chunk per workgroup (the hardware dispatcher balances chunks across
+// CUs and XCDs).  Phase 1 streams the chunk's full, aligned blocks through a
+// software pipeline: each wave keeps the loads of its next kDepth blocks in
+// flight while it stores and hashes the current one.  A block's expected hash
+// is loaded just before the block's data and folded into the wave reduction,
+// so comparing never waits on a load younger than the block itself (vmcnt
+// retires in order, and on CDNA it counts stores too).  Phase 2 handles the ragged last block and every block of
+// an unaligned entry with byte-granular code.  Restore and snapshot launches
+// reserve enough LDS to hold residency at one 8-wave workgroup per CU: about
+// eight deep streams per CU keep mixed read/write HBM traffic efficient.
 template <int OP, bool HASH>
 __global__ void __launch_bounds__(kThreads)
 k_stream(const Chunk *__restrict__ chunks, uint64_t count, gbyte *__restrict__ img_base,
          uint64_t img_origin, HashOut h)
 {
-    __shared__ uint64_t wave_part[kThreads / 64];
+    extern __shared__ uint64_t wave_part[];  // kWaves words used
     const uint32_t lane = threadIdx.x & 63;
     const uint32_t wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);  // wave-uniform
+    const uint64_t lane_g = 2ull * lane * kG;  // j*G offset of the lane's first word in a block
+    const bool check = HASH && h.expected != nullptr;
+    const uint64_t *const exp_dummy = (const uint64_t *)chunks;  // any readable word
 
     for (uint64_t ci = blockIdx.x; ci < count; ci += gridDim.x) {
         const Chunk c = chunks[ci];
         const uint32_t nblk = (c.len + kBlockBytes - 1) / kBlockBytes;
+        const uint32_t nfull = fast_blocks(c);
         const bool aligned = (c.addr & 15) == 0;
-        gbyte *const img = img_base + (c.img - img_origin);
+        gbyte *const img = img_base + (c.img - img_origin) + lane * 16;
+        gbyte *const ent = (gbyte *)c.addr + lane * 16;
+        gbyte *const src = OP == kRestore ? img : ent;
+        gbyte *const dst = OP == kRestore ? ent : img;
+        const uint64_t jg_chunk = (c.off >> 3) * kG + lane_g;
+        const uint64_t g0 = c.img >> 12;
         uint64_t tacc = 0;
 
-        for (uint32_t b = wave; b < nblk; b += kThreads / 64) {
-            const uint32_t boff = b * kBlockBytes;
-            gbyte *const ip = img + boff + lane * 16;
-            gbyte *const ep = (gbyte *)(c.addr + boff) + lane * 16;
-            // j*G of the lane's first word in segment 0
-            const uint64_t jg0 = (((c.off + boff) >> 3) + 2 * lane) * kG;
-            uint64_t hl = 0;
-
-            if (aligned && boff + kBlockBytes <= c.len) {
-                u32x4 v[4];
-                if (OP == kRestore) {
+        // ---- phase 1: full aligned blocks wave, wave + kWaves, ...
+        // A ring slot is consumed in place (stored and hashed straight from
+        // its registers) and only then reloaded with the wave's block kDepth
+        // steps ahead.  The expected-hash load is branch-free (a harmless
+        // address when not checking) and precedes its block's loads.  Both
+        // keep the compiler from inserting register copies that would wait
+        // for every outstanding load.
+        if (wave < nfull) {
+            const uint32_t mine = (nfull - wave + kWaves - 1) / kWaves;
+            u32x4 ring[kDepth][4];
+            uint64_t want[kDepth];
 #pragma unroll
-                    for (int k = 0; k < 4; ++k) v[k] = __builtin_nontemporal_load((const gvec *)(ip + k * 1024));
-#pragma unroll
-                    for (int k = 0; k < 4; ++k) __builtin_nontemporal_store(v[k], (gvec *)(ep + k * 1024));
-                } else {
-#pragma unroll
-                    for (int k = 0; k < 4; ++k) v[k] = __builtin_nontemporal_load((const gvec *)(ep + k * 1024));
-                    if (OP == kSnapshot) {
-#pragma unroll
-                        for (int k = 0; k < 4; ++k) __builtin_nontemporal_store(v[k], (gvec *)(ip + k * 1024));
-                    }
-                }
-                if (HASH) {
-#pragma unroll
-                    for (int k = 0; k < 4; ++k) hl ^= seg_hash(v[k], jg0 + (uint64_t)k * kSegStrideG);
-                }
-            } else {
-                // ragged last block and/or unaligned entry
-#pragma unroll
-                for (int k = 0; k < 4; ++k) {
-                    const uint32_t p = boff + k * 1024 + lane * 16;  // chunk-relative
-                    const uint32_t valid = p >= c.len ? 0u : min(16u, c.len - p);
-                    u32x4 v;
-                    if (OP == kRestore) {
-                        v = keep_bytes(*(const gvec *)(ip + k * 1024), valid);
-                        store_part(ep + k * 1024, v, valid, aligned);
-                    } else {
-                        v = load_part(ep + k * 1024, valid, aligned);
-                        if (OP == kSnapshot) *(gvec *)(ip + k * 1024) = v;
-                    }
-                    if (HASH) {
-                        const uint64_t jg = jg0 + (uint64_t)k * kSegStrideG;
-                        uint64_t w0 = (uint64_t)v.x | ((uint64_t)v.y << 32);
-                        uint64_t w1 = (uint64_t)v.z | ((uint64_t)v.w << 32);
-                        if (valid > 0) hl ^= mix64(w0 ^ jg);
-                        if (valid > 8) hl ^= mix64(w1 ^ (jg + kG));
-                    }
+            for (int d = 0; d < kDepth; ++d) {
+                if ((uint32_t)d < mine) {
+                    const uint32_t b = wave + d * kWaves;
+                    if (HASH) want[d] = *(check ? h.expected + g0 + b : exp_dummy);
+                    load_block(ring[d], src + (size_t)b * kBlockBytes);
                 }
             }
-
-            if (HASH) {
-                const uint64_t hb = wave_xor64(hl);
-                tacc ^= hb;
-                if (lane == 0) {
-                    const uint64_t gblk = (c.img >> 12) + b;
-                    if (h.blk) h.blk[gblk] = hb;
-                    if (h.expected && h.expected[gblk] != hb) {
-                        const uint64_t at = atomicAdd((unsigned long long *)h.mm_count, 1ull);
-                        if (h.mm_list && at < h.mm_cap) h.mm_list[at] = gblk;
+            for (uint32_t i = 0; i < mine; i += kDepth) {
+#pragma unroll
+                for (int d = 0; d < kDepth; ++d) {
+                    const uint32_t ii = i + d;
+                    if (ii >= mine) break;
+                    const uint32_t b = wave + ii * kWaves;
+                    if (OP != kVerify) store_block(ring[d], dst + (size_t)b * kBlockBytes);
+                    if (HASH) {
+                        const uint64_t jg0 = jg_chunk + (uint64_t)b * kBlockStrideG;
+                        uint64_t hl = 0;
+#pragma unroll
+                        for (int k = 0; k < 4; ++k) hl ^= seg_hash(ring[d][k], jg0 + (uint64_t)k * kSegStrideG);
+                        tacc ^= finish_block(hl, g0 + b, h, lane, check, want[d]);
+                    }
+                    if (ii + kDepth < mine) {
+                        const uint32_t nb = b + kDepth * kWaves;
+                        if (HASH) want[d] = *(check ? h.expected + g0 + nb : exp_dummy);
+                        load_block(ring[d], src + (size_t)nb * kBlockBytes);
                     }
                 }
             }
         }
 
+        // ---- phase 2: ragged last block and/or unaligned entry
+        for (uint32_t b = nfull + wave; b < nblk; b += kWaves) {
+            const uint32_t boff = b * kBlockBytes;
+            const uint64_t jg0 = jg_chunk + (uint64_t)b * kBlockStrideG;
+            uint64_t hl = 0;
+#pragma unroll
+            for (int k = 0; k < 4; ++k) {
+                const uint32_t p = boff + k * 1024 + lane * 16;  // chunk-relative
+                const uint32_t valid = p >= c.len ? 0u : min(16u, c.len - p);
+                u32x4 v;
+                if (OP == kRestore) {
+                    v = keep_bytes(*(const gvec *)(img + boff + k * 1024), valid);
+                    store_part(ent + boff + k * 1024, v, valid, aligned);
+                } else {
+                    v = load_part(ent + boff + k * 1024, valid, aligned);
+                    if (OP == kSnapshot) *(gvec *)(img + boff + k * 1024) = v;
+                }
+                if (HASH) {
+                    const uint64_t jg = jg0 + (uint64_t)k * kSegStrideG;
+                    uint64_t w0 = (uint64_t)v.x | ((uint64_t)v.y << 32);
+                    uint64_t w1 = (uint64_t)v.z | ((uint64_t)v.w << 32);
+                    if (valid > 0) hl ^= mix64(w0 ^ jg);
+                    if (valid > 8) hl ^= mix64(w1 ^ (jg + kG));
+                }
+            }
+            if (HASH) tacc ^= finish_block(hl, g0 + b, h, lane, check, check ? h.expected[g0 + b] : 0);
+        }
+
+        // ---- tensor hash: XOR of the eight waves' partials, one atomic per chunk
         if (HASH && h.ten) {
             if (lane == 0) wave_part[wave] = tacc;
             __syncthreads();
             if (threadIdx.x == 0) {
                 uint64_t t = 0;
 #pragma unroll
-                for (int w = 0; w < kThreads / 64; ++w) t ^= wave_part[w];
+                for (int w = 0; w < kWaves; ++w) t ^= wave_part[w];
                 if (t) atomicXor((unsigned long long *)(h.ten + c.entry), (unsigned long long)t);
             }
             __syncthreads();
@@ -227,13 +301,27 @@ k_prologue(uint64_t *__restrict__ ten, uint64_t n, uint64_t *__restrict__ mm_cou
 }
 
 constexpr uint64_t kMaxGrid = 1u << 20;
+// Dynamic LDS per workgroup: restore and snapshot ask for more than half of a
+// CU's 160 KiB so that one 8-wave workgroup is resident per CU; verify
+// (read-only) only needs the wave partials and runs at full occupancy.
+constexpr size_t kLdsCopy = 96 * 1024;
+constexpr size_t kLdsVerify = kWaves * sizeof(uint64_t);
 
 template <int OP, bool HASH>
 hipError_t launch_t(const Chunk *chunks, uint64_t first, uint64_t count, uint8_t *img_base,
                     uint64_t img_origin, const HashOut &h, hipStream_t s)
 {
+    const size_t lds = OP == kVerify ? kLdsVerify : kLdsCopy;
+    static std::once_flag attr_once;
+    static hipError_t attr_err = hipSuccess;
+    std::call_once(attr_once, [lds] {
+        if (lds > 64 * 1024)
+            attr_err = hipFuncSetAttribute((const void *)k_stream<OP, HASH>,
+                                           hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+    });
+    if (attr_err != hipSuccess) return attr_err;
     const uint64_t grid = count < kMaxGrid ? count : kMaxGrid;
-    hipLaunchKernelGGL((k_stream<OP, HASH>), dim3((uint32_t)grid), dim3(kThreads), 0, s, chunks + first, count,
+    hipLaunchKernelGGL((k_stream<OP, HASH>), dim3((uint32_t)grid), dim3(kThreads), lds, s, chunks + first, count,
                        (gbyte *)img_base, img_origin, h);
     return hipGetLastError();
 }
