@@ -204,6 +204,8 @@ def main():
         dst = torch.empty(1 << 30, dtype=torch.uint8, device="cuda")
         lt = timer.run(lambda: dst.copy_(gib, non_blocking=True), 10)
         link = (1 << 30) / statistics.median(lt) / 1e9
+        lt = timer.run(lambda: gib.copy_(dst, non_blocking=True), 10)
+        link_d2h = (1 << 30) / statistics.median(lt) / 1e9
         del dst
         ts = timer.run(lambda: gms.snapshot(m, pinned, m.image_bytes, gms.MEM_HOST_PINNED), 2)
         snap_h = statistics.median(ts)
@@ -223,7 +225,9 @@ def main():
             "restore_verify_ring_s": th, "restore_verify_ring_GB_s": P / th / 1e9,
             "link_frac": P / th / 1e9 / link,
             "restore_verify_zero_copy_s": tz, "restore_verify_zero_copy_GB_s": P / tz / 1e9,
+            "link_peak_d2h_GB_s": link_d2h,
             "snapshot_to_pinned_s": snap_h, "snapshot_to_pinned_GB_s": P / snap_h / 1e9,
+            "snapshot_link_frac": P / snap_h / 1e9 / link_d2h,
         }
         del pinned
 
