@@ -29,7 +29,7 @@ sys.path.insert(0, ROOT)
 
 METRIC = "restore+verify GB/s on 1 GPU; seconds to restore a 16 GB weight shard"
 HBM_PEAK_GBS = 8000.0
-ALL_ROWS = ["main", "snapshot", "plain", "verify", "h2d", "kv", "copy", "cpu"]
+ALL_ROWS = ["main", "snapshot", "plain", "verify", "h2d", "file", "kv", "copy", "cpu"]
 KERNEL_SOURCES = ["paper_2609_25451_amd/csrc/gms_kernels.hip", "paper_2609_25451_amd/csrc/gms_internal.h"]
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_restore_verify_llama8b.json")
 
@@ -219,6 +219,7 @@ def main():
         m.set_staging(0, 0)
         tz = statistics.median(timer.run(h2d, 2))
         assert int(hc.item()) == 0
+        snap_z = statistics.median(timer.run(lambda: gms.snapshot(m, pinned, m.image_bytes, gms.MEM_HOST_PINNED), 2))
         m.set_staging(64 << 20, 4)
         result_rows["h2d"] = {
             "link_peak_GB_s": link,
@@ -228,8 +229,12 @@ def main():
             "link_peak_d2h_GB_s": link_d2h,
             "snapshot_to_pinned_s": snap_h, "snapshot_to_pinned_GB_s": P / snap_h / 1e9,
             "snapshot_link_frac": P / snap_h / 1e9 / link_d2h,
+            "snapshot_to_pinned_zero_copy_GB_s": P / snap_z / 1e9,
         }
         del pinned
+
+    if "file" in rows:
+        result_rows["file"] = bench_file(torch, gms, m, expected)
 
     if "kv" in rows:
         result_rows["kv_pool"] = bench_kv(torch, np, gms, synth, timer)
@@ -285,6 +290,76 @@ def main():
         "rows": result_rows,
     }
     print(json.dumps(out), flush=True)
+
+
+def bench_file(torch, gms, m, expected):
+    """Cold repopulation from storage: the image written to a file, then streamed back."""
+    import shutil
+    import tempfile
+
+    d = tempfile.gettempdir()
+    free = shutil.disk_usage(d).free
+    if free < m.image_bytes + (2 << 30):
+        return {"skipped": f"{free} bytes free in {d}, need {m.image_bytes + (2 << 30)}"}
+    path = os.path.join(d, f"gms_bench_image_{os.getpid()}.bin")
+    cnt = torch.zeros(1, dtype=torch.int64, device="cuda")
+    out = {"dir": d, "bytes": m.image_bytes}
+    try:
+        t0 = time.perf_counter()
+        gms.snapshot_to_file(m, path, flags=gms.FILE_DIRECT | gms.FILE_SYNC)
+        torch.cuda.synchronize()
+        out["snapshot_direct_sync_s"] = time.perf_counter() - t0
+        out["storage_read_direct_GB_s"] = raw_direct_read(path, m.image_bytes) / 1e9
+        for label, flags in (("restore_verify_direct", gms.FILE_DIRECT), ("restore_verify_buffered_cold", 0),
+                             ("restore_verify_buffered_cached", 0)):
+            torch.cuda.synchronize()
+            t0 = time.perf_counter()
+            gms.restore_from_file(m, path, flags=flags, expected=expected, mismatch_count=cnt)
+            torch.cuda.synchronize()
+            t = time.perf_counter() - t0
+            assert int(cnt.item()) == 0, f"{label}: mismatches"
+            out[label + "_s"] = t
+            out[label + "_GB_s"] = m.payload_bytes / t / 1e9
+        out["storage_frac"] = out["restore_verify_direct_GB_s"] / out["storage_read_direct_GB_s"]
+        log(f"file restore+verify: direct {out['restore_verify_direct_GB_s']:.1f} GB/s "
+            f"(raw direct read {out['storage_read_direct_GB_s']:.1f} GB/s), "
+            f"cached {out['restore_verify_buffered_cached_GB_s']:.1f} GB/s")
+    finally:
+        if os.path.exists(path):
+            os.remove(path)
+    return out
+
+
+def raw_direct_read(path, nbytes, threads=8, piece=16 << 20):
+    """Bytes/s of plain parallel O_DIRECT reads of the file (the storage side alone)."""
+    import mmap
+    import threading
+
+    fd = os.open(path, os.O_RDONLY | getattr(os, "O_DIRECT", 0))
+    try:
+        per = -(-nbytes // threads)
+        per = -(-per // piece) * piece
+
+        def work(t):
+            buf = mmap.mmap(-1, piece)
+            lo, hi = t * per, min(nbytes, (t + 1) * per)
+            p = lo
+            while p < hi:
+                n = os.preadv(fd, [memoryview(buf)[: min(piece, hi - p)]], p)
+                if n <= 0:
+                    raise OSError("short read")
+                p += n
+            buf.close()
+
+        t0 = time.perf_counter()
+        ts = [threading.Thread(target=work, args=(t,)) for t in range(threads)]
+        for t in ts:
+            t.start()
+        for t in ts:
+            t.join()
+        return nbytes / (time.perf_counter() - t0)
+    finally:
+        os.close(fd)
 
 
 def bench_kv(torch, np, gms, synth, timer):

@@ -98,7 +98,8 @@ enum gms_status {
     GMS_ERR_SIZE = -3,    /* image (or output array) smaller than required */
     GMS_ERR_HIP = -4,     /* a HIP runtime call failed (see last error)     */
     GMS_ERR_NOMEM = -5,   /* host or device allocation failed              */
-    GMS_ERR_STATE = -6    /* data-plane call on a host-only manifest       */
+    GMS_ERR_STATE = -6,   /* data-plane call on a host-only manifest       */
+    GMS_ERR_IO = -7       /* a file could not be opened, read or written   */
 };
 
 enum gms_mem_kind {
@@ -141,13 +142,16 @@ int gms_manifest_device(const gms_manifest *m);
 int gms_layout(const gms_manifest *m, uint64_t *img_off, uint64_t *blk_base);
 
 /*
- * Staging ring for pinned-host images: `slots` device buffers of `slice_bytes`
- * (rounded down to a multiple of the chunk size, at least one chunk).  Host
- * slices are DMA'd into free slots on a library-owned copy stream while the
- * scatter/gather kernels drain filled slots on the caller's stream.
- * slots == 0 selects zero-copy: the kernels read/write the pinned image
- * directly over the host link.  Defaults: 64 MiB x 4.  Takes effect at the next
- * pinned-host call; frees the old ring after draining it.  Synchronous.
+ * Staging ring: `slots` device buffers of `slice_bytes` (rounded down to a
+ * multiple of the chunk size, at least one chunk).  A restore from a pinned
+ * host image DMAs host slices into free slots on a library-owned copy stream
+ * while the scatter kernel drains filled slots on the caller's stream; with
+ * slots == 0 it reads the pinned image directly over the host link
+ * (zero-copy) instead.  A snapshot into pinned host memory always writes it
+ * zero-copy.  The image-file calls also use the ring (and a pinned host ring
+ * of the same geometry) and need slots > 0.  Defaults: 64 MiB x 4.  Takes
+ * effect at the next ring call; frees the old rings after draining them.
+ * Synchronous.
  */
 int gms_manifest_set_staging(gms_manifest *m, uint64_t slice_bytes, uint32_t slots);
 
@@ -188,6 +192,42 @@ int gms_restore(const gms_manifest *m, const void *image, uint64_t image_bytes, 
 int gms_verify(const gms_manifest *m, const uint64_t *expected_blk, uint64_t *blk_hash_out,
                uint64_t *ten_hash_out, uint64_t *mismatch_count_out, uint64_t *mismatch_list_out,
                uint64_t mismatch_cap, void *stream);
+
+/* Flags of the image-file calls. */
+enum gms_file_flags {
+    GMS_FILE_DIRECT = 1, /* O_DIRECT I/O (bypasses the page cache) when the file system and
+                            the offset (multiple of 4096) allow it, buffered I/O otherwise */
+    GMS_FILE_SYNC = 2    /* snapshot: fsync the file before returning                      */
+};
+
+/*
+ * Cold repopulation from storage (paper section 3.3 and section 4: a
+ * replacement's model state is re-read from storage while its runtime is
+ * restored; section 3.1: the transfer costs S / B_eff).  The file holds the
+ * packed image (the layout above, no header) starting at `file_offset`.
+ * Each 64 MiB slice is read with `io_threads` parallel preads (0 = 8) into a
+ * pinned host slot, DMA'd into a device slot on the manifest's copy stream and
+ * scattered (and hashed / compared, as gms_restore) by the kernel on `stream`;
+ * a host slot is refilled once its DMA has finished.  The call returns when
+ * every slice has been read and enqueued; device work completes on `stream`.
+ * The first call allocates the manifest's pinned host ring (slots x slice).
+ * Errors: as gms_restore, plus GMS_ERR_IO (open/read failure) and
+ * GMS_ERR_SIZE (file shorter than file_offset + gms_image_bytes).
+ */
+int gms_restore_from_file(const gms_manifest *m, const char *path, uint64_t file_offset, uint32_t flags,
+                          uint32_t io_threads, const uint64_t *expected_blk, uint64_t *blk_hash_out,
+                          uint64_t *ten_hash_out, uint64_t *mismatch_count_out, uint64_t *mismatch_list_out,
+                          uint64_t mismatch_cap, void *stream);
+
+/*
+ * Writes the packed image to `path` (created or truncated), gathering on the
+ * device and draining the ring to the file with pwrite; optionally emits the
+ * block / tensor hashes of the gathered bytes.  Synchronous: the file is
+ * complete when the call returns (durable too with GMS_FILE_SYNC).
+ * Errors: GMS_ERR_STATE, GMS_ERR_INVALID, GMS_ERR_IO, GMS_ERR_HIP, GMS_ERR_NOMEM.
+ */
+int gms_snapshot_to_file(const gms_manifest *m, const char *path, uint32_t flags, uint32_t io_threads,
+                         uint64_t *blk_hash_out, uint64_t *ten_hash_out, void *stream);
 
 /* Static description of a status code. */
 const char *gms_status_str(int status);

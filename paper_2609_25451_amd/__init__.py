@@ -38,6 +38,9 @@ GMS_ERR_SIZE = -3
 GMS_ERR_HIP = -4
 GMS_ERR_NOMEM = -5
 GMS_ERR_STATE = -6
+GMS_ERR_IO = -7
+FILE_DIRECT = 1
+FILE_SYNC = 2
 MEM_DEVICE = 0
 MEM_HOST_PINNED = 1
 HOST_ONLY = -1
@@ -68,6 +71,9 @@ _set_staging = _sig("gms_manifest_set_staging", INT, [VP, U64, ctypes.c_uint32])
 _snapshot = _sig("gms_snapshot", INT, [VP, VP, U64, INT, VP, VP, VP])
 _restore = _sig("gms_restore", INT, [VP, VP, U64, INT, VP, VP, VP, VP, VP, U64, VP])
 _verify = _sig("gms_verify", INT, [VP, VP, VP, VP, VP, VP, U64, VP])
+_restore_file = _sig("gms_restore_from_file", INT,
+                     [VP, ctypes.c_char_p, U64, ctypes.c_uint32, ctypes.c_uint32, VP, VP, VP, VP, VP, U64, VP])
+_snapshot_file = _sig("gms_snapshot_to_file", INT, [VP, ctypes.c_char_p, ctypes.c_uint32, ctypes.c_uint32, VP, VP, VP])
 _status_str = _sig("gms_status_str", ctypes.c_char_p, [INT])
 _last_error = _sig("gms_last_error", ctypes.c_char_p, [])
 _abi = _sig("gms_abi_version", INT, [])
@@ -204,6 +210,20 @@ def verify(m: Manifest, expected=None, blk_hash=None, ten_hash=None, mismatch_co
                    _ptr(mismatch_list), mismatch_cap, _stream(stream)), "gms_verify")
 
 
+def restore_from_file(m: Manifest, path, file_offset: int = 0, flags: int = FILE_DIRECT, io_threads: int = 0,
+                      expected=None, blk_hash=None, ten_hash=None, mismatch_count=None, mismatch_list=None,
+                      mismatch_cap: int = 0, stream=None) -> None:
+    _check(_restore_file(m._h, os.fsencode(path), file_offset, flags, io_threads, _ptr(expected), _ptr(blk_hash),
+                         _ptr(ten_hash), _ptr(mismatch_count), _ptr(mismatch_list), mismatch_cap, _stream(stream)),
+           "gms_restore_from_file")
+
+
+def snapshot_to_file(m: Manifest, path, flags: int = 0, io_threads: int = 0, blk_hash=None, ten_hash=None,
+                     stream=None) -> None:
+    _check(_snapshot_file(m._h, os.fsencode(path), flags, io_threads, _ptr(blk_hash), _ptr(ten_hash),
+                          _stream(stream)), "gms_snapshot_to_file")
+
+
 def status_str(rc: int) -> str:
     return _status_str(rc).decode()
 
@@ -215,6 +235,8 @@ gms_snapshot = _snapshot
 gms_restore = _restore
 gms_verify = _verify
 gms_layout = _layout
+gms_restore_from_file = _restore_file
+gms_snapshot_to_file = _snapshot_file
 gms_manifest_set_staging = _set_staging
 gms_status_str = _status_str
 gms_last_error = _last_error

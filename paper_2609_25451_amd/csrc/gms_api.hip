@@ -11,15 +11,23 @@
 #include <string>
 #include <vector>
 
-#include "gms.h"
-#include "gms_internal.h"
+#include "gms_host.h"
 
 using gms::Chunk;
 using gms::HashOut;
+using gms::ceil_div;
+using gms::DeviceGuard;
+using gms::fail;
+using gms::fail_hip;
+using gms::kMaxChunk;
+using gms::kDefaultSlice;
+using gms::kMaxSlots;
 
 namespace {
-
 thread_local std::string g_last_error;
+}  // namespace
+
+namespace gms {
 
 int fail(int status, const char *fmt, ...)
 {
@@ -37,58 +45,7 @@ int fail_hip(hipError_t e, const char *what)
     return fail(GMS_ERR_HIP, "%s: %s (%d)", what, hipGetErrorString(e), (int)e);
 }
 
-constexpr uint64_t kMaxChunk = 64ull << 20;
-constexpr uint64_t kDefaultSlice = 64ull << 20;
-constexpr uint32_t kDefaultSlots = 4;
-constexpr uint32_t kMaxSlots = 16;
-
-uint64_t ceil_div(uint64_t a, uint64_t b) { return a / b + (a % b != 0); }
-
-// Makes `device` current for the lifetime of the guard, restoring the
-// caller's current device afterwards.
-struct DeviceGuard {
-    int prev = -1;
-    hipError_t err = hipSuccess;
-    explicit DeviceGuard(int device)
-    {
-        err = hipGetDevice(&prev);
-        if (err == hipSuccess && prev != device) err = hipSetDevice(device);
-    }
-    ~DeviceGuard()
-    {
-        int cur = -1;
-        if (prev >= 0 && hipGetDevice(&cur) == hipSuccess && cur != prev) (void)hipSetDevice(prev);
-    }
-};
-
-}  // namespace
-
-struct gms_manifest {
-    int device = GMS_HOST_ONLY;
-    uint64_t n = 0;
-    uint64_t chunk_bytes = 0;
-    uint64_t payload = 0, image_bytes = 0, num_blocks = 0;
-    std::vector<uint64_t> img_off;
-    std::vector<Chunk> chunks;  // host copy, sorted by image offset
-    Chunk *d_chunks = nullptr;
-
-    // staging ring (pinned-host images); created lazily
-    std::mutex ring_mu;
-    uint64_t slice_bytes = kDefaultSlice;
-    uint32_t slots = kDefaultSlots;
-    uint8_t *d_ring = nullptr;
-    uint64_t ring_slice = 0;
-    uint32_t ring_slots = 0;
-    hipStream_t copy_stream = nullptr;
-    hipEvent_t ev_filled[kMaxSlots] = {};
-    hipEvent_t ev_free[kMaxSlots] = {};
-    hipEvent_t ev_entry = nullptr;
-    hipEvent_t ev_done = nullptr;
-    bool done_recorded = false;
-    std::vector<uint64_t> slice_first;  // per slice: first chunk index; back() = #chunks
-};
-
-namespace {
+void clear_error() { g_last_error.clear(); }
 
 void free_ring(gms_manifest *m)
 {
@@ -97,8 +54,11 @@ void free_ring(gms_manifest *m)
     for (uint32_t i = 0; i < kMaxSlots; ++i) {
         if (m->ev_filled[i]) (void)hipEventDestroy(m->ev_filled[i]);
         if (m->ev_free[i]) (void)hipEventDestroy(m->ev_free[i]);
-        m->ev_filled[i] = m->ev_free[i] = nullptr;
+        if (m->ev_host[i]) (void)hipEventDestroy(m->ev_host[i]);
+        m->ev_filled[i] = m->ev_free[i] = m->ev_host[i] = nullptr;
     }
+    if (m->h_ring) (void)hipHostFree(m->h_ring);
+    m->h_ring = nullptr;
     if (m->ev_entry) (void)hipEventDestroy(m->ev_entry);
     if (m->ev_done) (void)hipEventDestroy(m->ev_done);
     if (m->copy_stream) (void)hipStreamDestroy(m->copy_stream);
@@ -136,7 +96,8 @@ int ensure_ring(gms_manifest *m)
         return free_ring(m), fail_hip(e, "staging ring: hipStreamCreate");
     for (uint32_t i = 0; i < m->slots; ++i) {
         if ((e = hipEventCreateWithFlags(&m->ev_filled[i], hipEventDisableTiming)) != hipSuccess ||
-            (e = hipEventCreateWithFlags(&m->ev_free[i], hipEventDisableTiming)) != hipSuccess)
+            (e = hipEventCreateWithFlags(&m->ev_free[i], hipEventDisableTiming)) != hipSuccess ||
+            (e = hipEventCreateWithFlags(&m->ev_host[i], hipEventDisableTiming)) != hipSuccess)
             return free_ring(m), fail_hip(e, "staging ring: hipEventCreate");
     }
     if ((e = hipEventCreateWithFlags(&m->ev_entry, hipEventDisableTiming)) != hipSuccess ||
@@ -151,6 +112,22 @@ int ensure_ring(gms_manifest *m)
     for (uint64_t s = 0; s < nslices; ++s) {
         while (ci < m->chunks.size() && m->chunks[ci].img < s * slice) ++ci;
         m->slice_first[s] = ci;
+    }
+    return GMS_OK;
+}
+
+int ensure_host_ring(gms_manifest *m)
+{
+    int rc = ensure_ring(m);
+    if (rc != GMS_OK) return rc;
+    if (!m->d_ring) return fail(GMS_ERR_STATE, "file paths need the staging ring (slots > 0)");
+    if (m->h_ring) return GMS_OK;
+    hipError_t e = hipHostMalloc((void **)&m->h_ring, m->ring_slice * m->ring_slots, hipHostMallocDefault);
+    if (e != hipSuccess) {
+        m->h_ring = nullptr;
+        (void)hipGetLastError();
+        return fail(GMS_ERR_NOMEM, "pinned host ring: hipHostMalloc(%llu) failed: %s",
+                    (unsigned long long)(m->ring_slice * m->ring_slots), hipGetErrorString(e));
     }
     return GMS_OK;
 }
@@ -239,6 +216,15 @@ HashOut make_hash(const uint64_t *expected, uint64_t *blk, uint64_t *ten, uint64
     return h;
 }
 
+}  // namespace gms
+
+namespace {
+
+using gms::make_hash;
+using gms::check_common;
+using gms::check_outputs;
+using gms::ensure_ring;
+
 // Device-resident image, or zero-copy access to a pinned one: one launch.
 int run_direct(const gms_manifest *m, int op, uint8_t *image, const HashOut &h, hipStream_t s)
 {
@@ -246,11 +232,10 @@ int run_direct(const gms_manifest *m, int op, uint8_t *image, const HashOut &h, 
     return e == hipSuccess ? GMS_OK : fail_hip(e, "kernel launch");
 }
 
-// Pinned image through the staging ring.  Restore: DMA slice -> slot on the
-// copy stream, scatter slot -> entries on the caller's stream.  Snapshot:
-// gather entries -> slot on the caller's stream, DMA slot -> slice on the
-// copy stream; the caller's stream finally waits for the last DMA.
-int run_ring(gms_manifest *m, int op, uint8_t *host_image, const HashOut &h, hipStream_t s)
+// Pinned image restored through the staging ring: DMA slice -> device slot on
+// the copy stream, scatter slot -> entries on the caller's stream, and the
+// copy stream refills a slot only after the kernel that read it.
+int run_ring(gms_manifest *m, const HashOut &h, uint8_t *host_image, hipStream_t s)
 {
     int rc = ensure_ring(m);
     if (rc != GMS_OK) return rc;
@@ -276,33 +261,23 @@ int run_ring(gms_manifest *m, int op, uint8_t *host_image, const HashOut &h, hip
         const uint64_t lo = sl * slice;
         const uint64_t bytes = std::min(slice, m->image_bytes - lo);
         const uint64_t c0 = m->slice_first[sl], c1 = m->slice_first[sl + 1];
-        if (op == gms::kRestore) {
-            if (sl >= k) GMS_TRY(hipStreamWaitEvent(m->copy_stream, m->ev_free[slot], 0));
-            GMS_TRY(hipMemcpyAsync(dev, host_image + lo, bytes, hipMemcpyHostToDevice, m->copy_stream));
-            GMS_TRY(hipEventRecord(m->ev_filled[slot], m->copy_stream));
-            GMS_TRY(hipStreamWaitEvent(s, m->ev_filled[slot], 0));
-            GMS_TRY(gms::launch_stream(op, h.any(), m->d_chunks, c0, c1 - c0, dev, lo, h, s));
-            GMS_TRY(hipEventRecord(m->ev_free[slot], s));
-        } else {
-            if (sl >= k) GMS_TRY(hipStreamWaitEvent(s, m->ev_free[slot], 0));
-            GMS_TRY(gms::launch_stream(op, h.any(), m->d_chunks, c0, c1 - c0, dev, lo, h, s));
-            GMS_TRY(hipEventRecord(m->ev_filled[slot], s));
-            GMS_TRY(hipStreamWaitEvent(m->copy_stream, m->ev_filled[slot], 0));
-            GMS_TRY(hipMemcpyAsync(host_image + lo, dev, bytes, hipMemcpyDeviceToHost, m->copy_stream));
-            GMS_TRY(hipEventRecord(m->ev_free[slot], m->copy_stream));
-        }
+        if (sl >= k) GMS_TRY(hipStreamWaitEvent(m->copy_stream, m->ev_free[slot], 0));
+        GMS_TRY(hipMemcpyAsync(dev, host_image + lo, bytes, hipMemcpyHostToDevice, m->copy_stream));
+        GMS_TRY(hipEventRecord(m->ev_filled[slot], m->copy_stream));
+        GMS_TRY(hipStreamWaitEvent(s, m->ev_filled[slot], 0));
+        GMS_TRY(gms::launch_stream(gms::kRestore, h.any(), m->d_chunks, c0, c1 - c0, dev, lo, h, s));
+        GMS_TRY(hipEventRecord(m->ev_free[slot], s));
     }
-    if (op == gms::kSnapshot) {
-        GMS_TRY(hipEventRecord(m->ev_done, m->copy_stream));
-        GMS_TRY(hipStreamWaitEvent(s, m->ev_done, 0));
-    } else {
-        GMS_TRY(hipEventRecord(m->ev_done, s));
-    }
+    GMS_TRY(hipEventRecord(m->ev_done, s));
     m->done_recorded = true;
 #undef GMS_TRY
     return GMS_OK;
 }
 
+// Device images take one launch.  A pinned image is written by a snapshot
+// with zero-copy stores straight over the host link (steadier and faster than
+// a device slot plus DMA) and read by a restore through the staging ring, or
+// zero-copy when the manifest has no ring slots.
 int run_op(const gms_manifest *cm, int op, void *image, int kind, const HashOut &h, void *stream)
 {
     gms_manifest *m = const_cast<gms_manifest *>(cm);
@@ -314,17 +289,24 @@ int run_op(const gms_manifest *cm, int op, void *image, int kind, const HashOut 
     if (m->chunks.empty()) return GMS_OK;
     if (op == gms::kVerify || kind == GMS_MEM_DEVICE) return run_direct(m, op, (uint8_t *)image, h, s);
     std::lock_guard<std::mutex> lock(m->ring_mu);
-    if (m->slots == 0) {
-        // zero-copy: the kernels address the pinned image through its device mapping
+    if (op == gms::kSnapshot || m->slots == 0) {
         void *dev = nullptr;
-        hipError_t e2 = hipHostGetDevicePointer(&dev, image, 0);
-        if (e2 != hipSuccess) return fail_hip(e2, "hipHostGetDevicePointer");
+        e = hipHostGetDevicePointer(&dev, image, 0);
+        if (e != hipSuccess) return fail_hip(e, "hipHostGetDevicePointer");
+        if (m->done_recorded && (e = hipStreamWaitEvent(s, m->ev_done, 0)) != hipSuccess)
+            return fail_hip(e, "ring order");
         return run_direct(m, op, (uint8_t *)dev, h, s);
     }
-    return run_ring(m, op, (uint8_t *)image, h, s);
+    return run_ring(m, h, (uint8_t *)image, s);
 }
 
 }  // namespace
+
+using gms::check_common;
+using gms::check_device_range;
+using gms::check_outputs;
+using gms::free_ring;
+using gms::make_hash;
 
 extern "C" {
 
@@ -340,6 +322,7 @@ const char *gms_status_str(int status)
     case GMS_ERR_HIP: return "HIP runtime error";
     case GMS_ERR_NOMEM: return "out of memory";
     case GMS_ERR_STATE: return "operation not valid for this manifest";
+    case GMS_ERR_IO: return "file I/O error";
     default: return "unknown status";
     }
 }
@@ -349,7 +332,7 @@ const char *gms_last_error(void) { return g_last_error.c_str(); }
 int gms_manifest_create(const gms_entry *entries, uint64_t n, int device, uint64_t chunk_bytes,
                         gms_manifest **out)
 {
-    g_last_error.clear();
+    gms::clear_error();
     if (!out) return fail(GMS_ERR_INVALID, "out is null");
     *out = nullptr;
     if (n && !entries) return fail(GMS_ERR_INVALID, "entries is null");
@@ -506,7 +489,7 @@ int gms_manifest_set_staging(gms_manifest *m, uint64_t slice_bytes, uint32_t slo
 int gms_snapshot(const gms_manifest *m, void *image, uint64_t image_bytes, int image_kind, uint64_t *blk_hash_out,
                  uint64_t *ten_hash_out, void *stream)
 {
-    g_last_error.clear();
+    gms::clear_error();
     int rc = check_common(m, image, image_bytes, image_kind, true);
     if (rc != GMS_OK) return rc;
     HashOut h = make_hash(nullptr, blk_hash_out, ten_hash_out, nullptr, nullptr, 0);
@@ -518,7 +501,7 @@ int gms_restore(const gms_manifest *m, const void *image, uint64_t image_bytes, 
                 const uint64_t *expected_blk, uint64_t *blk_hash_out, uint64_t *ten_hash_out,
                 uint64_t *mismatch_count_out, uint64_t *mismatch_list_out, uint64_t mismatch_cap, void *stream)
 {
-    g_last_error.clear();
+    gms::clear_error();
     int rc = check_common(m, image, image_bytes, image_kind, true);
     if (rc != GMS_OK) return rc;
     HashOut h = make_hash(expected_blk, blk_hash_out, ten_hash_out, mismatch_count_out, mismatch_list_out,
@@ -530,7 +513,7 @@ int gms_restore(const gms_manifest *m, const void *image, uint64_t image_bytes, 
 int gms_verify(const gms_manifest *m, const uint64_t *expected_blk, uint64_t *blk_hash_out, uint64_t *ten_hash_out,
                uint64_t *mismatch_count_out, uint64_t *mismatch_list_out, uint64_t mismatch_cap, void *stream)
 {
-    g_last_error.clear();
+    gms::clear_error();
     int rc = check_common(m, nullptr, 0, GMS_MEM_DEVICE, false);
     if (rc != GMS_OK) return rc;
     HashOut h = make_hash(expected_blk, blk_hash_out, ten_hash_out, mismatch_count_out, mismatch_list_out,

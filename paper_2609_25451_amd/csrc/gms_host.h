@@ -1,0 +1,85 @@
+// Host-side internals shared by the C-ABI implementation files (gms_api.hip,
+// gms_file.hip): the manifest object, error reporting and the helpers that
+// validate arguments and drive the staging rings.  Not installed.
+#pragma once
+
+#include <cstdint>
+#include <mutex>
+#include <string>
+#include <vector>
+
+#include "gms.h"
+#include "gms_internal.h"
+
+namespace gms {
+
+constexpr uint64_t kMaxChunk = 64ull << 20;
+constexpr uint64_t kDefaultSlice = 64ull << 20;
+constexpr uint32_t kDefaultSlots = 4;
+constexpr uint32_t kMaxSlots = 16;
+
+inline uint64_t ceil_div(uint64_t a, uint64_t b) { return a / b + (a % b != 0); }
+
+// Records a message for gms_last_error() and returns `status`.
+int fail(int status, const char *fmt, ...) __attribute__((format(printf, 2, 3)));
+int fail_hip(hipError_t e, const char *what);
+void clear_error();
+
+// Makes `device` current for the lifetime of the guard, restoring the
+// caller's current device afterwards.
+struct DeviceGuard {
+    int prev = -1;
+    hipError_t err = hipSuccess;
+    explicit DeviceGuard(int device)
+    {
+        err = hipGetDevice(&prev);
+        if (err == hipSuccess && prev != device) err = hipSetDevice(device);
+    }
+    ~DeviceGuard()
+    {
+        int cur = -1;
+        if (prev >= 0 && hipGetDevice(&cur) == hipSuccess && cur != prev) (void)hipSetDevice(prev);
+    }
+};
+
+}  // namespace gms
+
+struct gms_manifest {
+    int device = GMS_HOST_ONLY;
+    uint64_t n = 0;
+    uint64_t chunk_bytes = 0;
+    uint64_t payload = 0, image_bytes = 0, num_blocks = 0;
+    std::vector<uint64_t> img_off;
+    std::vector<gms::Chunk> chunks;  // host copy, sorted by image offset
+    gms::Chunk *d_chunks = nullptr;
+
+    // staging rings, created lazily: device slots for pinned-host images, and
+    // pinned host slots for image files.  ring_mu serialises their users.
+    std::mutex ring_mu;
+    uint64_t slice_bytes = gms::kDefaultSlice;
+    uint32_t slots = gms::kDefaultSlots;
+    uint8_t *d_ring = nullptr;
+    uint64_t ring_slice = 0;
+    uint32_t ring_slots = 0;
+    uint8_t *h_ring = nullptr;  // pinned host slots (file paths only)
+    hipStream_t copy_stream = nullptr;
+    hipEvent_t ev_filled[gms::kMaxSlots] = {};
+    hipEvent_t ev_free[gms::kMaxSlots] = {};
+    hipEvent_t ev_host[gms::kMaxSlots] = {};  // DMA that last touched a host slot finished
+    hipEvent_t ev_entry = nullptr;
+    hipEvent_t ev_done = nullptr;
+    bool done_recorded = false;
+    std::vector<uint64_t> slice_first;  // per slice: first chunk index; back() = #chunks
+};
+
+namespace gms {
+
+void free_ring(gms_manifest *m);
+int ensure_ring(gms_manifest *m);       // device slots, copy stream, events, slice table
+int ensure_host_ring(gms_manifest *m);  // plus pinned host slots
+int check_common(const gms_manifest *m, const void *image, uint64_t image_bytes, int kind, bool need_image);
+int check_outputs(const gms_manifest *m, const HashOut &h);
+HashOut make_hash(const uint64_t *expected, uint64_t *blk, uint64_t *ten, uint64_t *cnt, uint64_t *list,
+                  uint64_t cap);
+
+}  // namespace gms

@@ -311,10 +311,10 @@ template <int OP, bool HASH>
 hipError_t launch_t(const Chunk *chunks, uint64_t first, uint64_t count, uint8_t *img_base,
                     uint64_t img_origin, const HashOut &h, hipStream_t s)
 {
-    const size_t lds = OP == kVerify ? kLdsVerify : kLdsCopy;
+    constexpr size_t lds = OP == kVerify ? kLdsVerify : kLdsCopy;
     static std::once_flag attr_once;
     static hipError_t attr_err = hipSuccess;
-    std::call_once(attr_once, [lds] {
+    std::call_once(attr_once, [] {
         if (lds > 64 * 1024)
             attr_err = hipFuncSetAttribute((const void *)k_stream<OP, HASH>,
                                            hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);

@@ -113,6 +113,11 @@ def test_data_plane_refused_on_host_only_manifest():
     with pytest.raises(gms.GmsError) as e:
         m.set_staging(1 << 20, 2)
     assert e.value.status == gms.GMS_ERR_STATE
+    for call in (lambda: gms.restore_from_file(m, "/nonexistent"),
+                 lambda: gms.snapshot_to_file(m, "/nonexistent")):
+        with pytest.raises(gms.GmsError) as e:
+            call()
+        assert e.value.status == gms.GMS_ERR_STATE
 
 
 def test_null_arguments():
@@ -123,5 +128,9 @@ def test_null_arguments():
     assert gms.gms_restore(None, None, 0, 0, None, None, None, None, None, 0, None) == gms.GMS_ERR_INVALID
     assert gms.gms_verify(None, None, None, None, None, None, 0, None) == gms.GMS_ERR_INVALID
     assert b"null" in gms.gms_last_error()
-    for rc in (0, -1, -2, -3, -4, -5, -6, 7):
+    assert gms.gms_restore_from_file(None, b"x", 0, 0, 0, None, None, None, None, None, 0, None) == gms.GMS_ERR_INVALID
+    assert gms.gms_snapshot_to_file(None, b"x", 0, 0, None, None, None) == gms.GMS_ERR_INVALID
+    m = gms.Manifest([(4096, 10)], device=gms.HOST_ONLY)
+    assert gms.gms_restore_from_file(m.handle, None, 0, 0, 0, None, None, None, None, None, 0, None) == gms.GMS_ERR_STATE
+    for rc in (0, -1, -2, -3, -4, -5, -6, -7, 7):
         assert gms.status_str(rc)
