@@ -29,7 +29,7 @@ sys.path.insert(0, ROOT)
 
 METRIC = "restore+verify GB/s on 1 GPU; seconds to restore a 16 GB weight shard"
 HBM_PEAK_GBS = 8000.0
-ALL_ROWS = ["main", "snapshot", "plain", "verify", "h2d", "file", "kv", "copy", "cpu"]
+ALL_ROWS = ["main", "snapshot", "plain", "verify", "h2d", "file", "kv", "kv_vmm", "copy", "cpu"]
 KERNEL_SOURCES = ["paper_2609_25451_amd/csrc/gms_kernels.hip", "paper_2609_25451_amd/csrc/gms_internal.h"]
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_restore_verify_llama8b.json")
 
@@ -238,6 +238,8 @@ def main():
 
     if "kv" in rows:
         result_rows["kv_pool"] = bench_kv(torch, np, gms, synth, timer)
+    if "kv_vmm" in rows:
+        result_rows["kv_pool_vmm"] = bench_kv_vmm(torch, np, gms, synth, timer)
 
     # ---------------------------------------------------------------- roofline
     roof = None
@@ -400,6 +402,42 @@ def bench_kv(torch, np, gms, synth, timer):
     return {"entries": m.num_entries, "payload_bytes": P, "s": t, "GB_s": P / t / 1e9,
             "hbm_frac": 2 * P / t / 1e9 / HBM_PEAK_GBS, "mismatches": c, "flagged": flagged,
             "planted_block": int(base[e] + blk), "dead_units_untouched_first4_layers": dead_ok}
+
+
+def bench_kv_vmm(torch, np, gms, synth, timer):
+    """The 8 GiB KV pool in VMM slabs: pages released and remapped at the same
+    addresses, then the live blocks restored (and verified) into the fresh pages."""
+    p = synth.kv_pool()
+    pool = gms.Pool(va_bytes=p.layers * p.layer_bytes + (1 << 30), slab_bytes=p.layer_bytes)
+    try:
+        kv = [pool.alloc(p.layer_bytes) for _ in range(p.layers)]
+        for l, a in enumerate(kv):
+            synth.dev_fill_bf16(a, p.layer_bytes // 2, p.seed, l)
+        live = synth.live_map(p.blocks, p.n_live, p.map_seed, p.map_stream)
+        ents = [(kv[l] + int(b) * p.unit_bytes, p.unit_bytes) for l in range(p.layers) for b in live]
+        m = gms.Manifest(ents, device=0)
+        img = torch.empty(m.image_bytes, dtype=torch.uint8, device="cuda")
+        exp = torch.zeros(m.num_blocks, dtype=torch.int64, device="cuda")
+        gms.snapshot(m, img, m.image_bytes, blk_hash=exp)
+        torch.cuda.synchronize()
+        span = p.layers * p.layer_bytes
+        t0 = time.perf_counter()
+        pool.release(kv[0], span)
+        t_rel = time.perf_counter() - t0
+        t0 = time.perf_counter()
+        pool.remap(kv[0], span)
+        t_map = time.perf_counter() - t0
+        cnt = torch.zeros(1, dtype=torch.int64, device="cuda")
+        ts = timer.run(lambda: gms.restore(m, img, m.image_bytes, expected=exp, mismatch_count=cnt), 5)
+        assert int(cnt.item()) == 0
+        t = statistics.median(ts)
+        payload = m.payload_bytes
+        m.close()
+        return {"pool_bytes": span, "release_s": t_rel, "remap_s": t_map, "restore_verify_s": t,
+                "restore_verify_GB_s": payload / t / 1e9, "hbm_frac": 2 * payload / t / 1e9 / HBM_PEAK_GBS,
+                "mappings": pool.info()["mappings"]}
+    finally:
+        pool.close()
 
 
 def bench_cpu(torch, np, image, m, specs):

@@ -229,6 +229,60 @@ int gms_restore_from_file(const gms_manifest *m, const char *path, uint64_t file
 int gms_snapshot_to_file(const gms_manifest *m, const char *path, uint32_t flags, uint32_t io_threads,
                          uint64_t *blk_hash_out, uint64_t *ten_hash_out, void *stream);
 
+/*
+ * Device memory pool over HIP virtual memory (paper section 4: a first-fit
+ * suballocator over 2 GiB slabs, with dedicated slabs for larger allocations,
+ * so that mapping and access changes happen per slab rather than per tensor;
+ * section 3.2: shared state is mapped read-only for readers; sections 3.1 and
+ * 3.3: KV pages are released before a checkpoint while their virtual
+ * addresses stay reserved, and fresh pages are mapped at the same addresses
+ * after restore).  One VA reservation of `va_bytes` holds every mapping.
+ * A mapping (a slab, or a dedicated mapping for an allocation larger than a
+ * slab) is the unit of release, remap and access change.  Addresses handed
+ * out stay valid for the pool's lifetime, across release and remap, and can
+ * be used in manifests like any device allocation.  The caller must not let
+ * kernels (including snapshot/restore/verify) touch a released range; release
+ * synchronises the device first.  Not for use under graph capture.
+ */
+typedef struct gms_pool gms_pool;
+
+/* Reserves va_bytes of device VA on `device`; slab_bytes 0 = 2 GiB.  Both must be
+ * multiples of the allocation granularity (gms_pool_info).  Errors: GMS_ERR_INVALID,
+ * GMS_ERR_STATE (no VMM support), GMS_ERR_NOMEM, GMS_ERR_HIP. */
+int gms_pool_create(int device, uint64_t va_bytes, uint64_t slab_bytes, gms_pool **out);
+
+/* Unmaps and releases every mapping and frees the reservation.  NULL is a no-op. */
+void gms_pool_destroy(gms_pool *p);
+
+/* First fit in mapped slabs (a new slab is mapped when none fits); an allocation larger
+ * than a slab gets a dedicated mapping.  align: power of two <= granularity, 0 = 256.
+ * Errors: GMS_ERR_INVALID, GMS_ERR_NOMEM (reservation or device memory exhausted). */
+int gms_pool_alloc(gms_pool *p, uint64_t bytes, uint64_t align, uint64_t *addr_out);
+
+/* Returns an allocation; a dedicated mapping is unmapped and released (its VA stays
+ * reserved).  Errors: GMS_ERR_INVALID (not an allocation of this pool). */
+int gms_pool_free(gms_pool *p, uint64_t addr);
+
+/* Releases the physical pages of the mappings that exactly tile [addr, addr+bytes),
+ * keeping their VA; allocations inside keep their addresses. */
+int gms_pool_release(gms_pool *p, uint64_t addr, uint64_t bytes);
+
+/* Backs released mappings in [addr, addr+bytes) with fresh physical pages at the same
+ * VA, read-write.  Contents are undefined until written. */
+int gms_pool_remap(gms_pool *p, uint64_t addr, uint64_t bytes);
+
+/* Device access to the mapped mappings tiling [addr, addr+bytes): read_only != 0 maps
+ * them read-only, 0 read-write.  Errors: GMS_ERR_INVALID, GMS_ERR_STATE (released). */
+int gms_pool_set_access(gms_pool *p, uint64_t addr, uint64_t bytes, int read_only);
+
+/* Pool facts; any output may be NULL. */
+int gms_pool_info(const gms_pool *p, uint64_t *base, uint64_t *reserved, uint64_t *mapped_bytes,
+                  uint64_t *mappings, uint64_t *granularity);
+
+/* The mapping holding addr: its start, size and whether it is currently backed. */
+int gms_pool_mapping_of(const gms_pool *p, uint64_t addr, uint64_t *map_addr, uint64_t *map_bytes,
+                        int *mapped);
+
 /* Static description of a status code. */
 const char *gms_status_str(int status);
 

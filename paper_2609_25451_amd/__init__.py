@@ -74,6 +74,15 @@ _verify = _sig("gms_verify", INT, [VP, VP, VP, VP, VP, VP, U64, VP])
 _restore_file = _sig("gms_restore_from_file", INT,
                      [VP, ctypes.c_char_p, U64, ctypes.c_uint32, ctypes.c_uint32, VP, VP, VP, VP, VP, U64, VP])
 _snapshot_file = _sig("gms_snapshot_to_file", INT, [VP, ctypes.c_char_p, ctypes.c_uint32, ctypes.c_uint32, VP, VP, VP])
+_pool_create = _sig("gms_pool_create", INT, [INT, U64, U64, ctypes.POINTER(VP)])
+_pool_destroy = _sig("gms_pool_destroy", None, [VP])
+_pool_alloc = _sig("gms_pool_alloc", INT, [VP, U64, U64, ctypes.POINTER(U64)])
+_pool_free = _sig("gms_pool_free", INT, [VP, U64])
+_pool_release = _sig("gms_pool_release", INT, [VP, U64, U64])
+_pool_remap = _sig("gms_pool_remap", INT, [VP, U64, U64])
+_pool_set_access = _sig("gms_pool_set_access", INT, [VP, U64, U64, INT])
+_pool_info = _sig("gms_pool_info", INT, [VP, VP, VP, VP, VP, VP])
+_pool_mapping_of = _sig("gms_pool_mapping_of", INT, [VP, U64, VP, VP, VP])
 _status_str = _sig("gms_status_str", ctypes.c_char_p, [INT])
 _last_error = _sig("gms_last_error", ctypes.c_char_p, [])
 _abi = _sig("gms_abi_version", INT, [])
@@ -224,6 +233,55 @@ def snapshot_to_file(m: Manifest, path, flags: int = 0, io_threads: int = 0, blk
                           _stream(stream)), "gms_snapshot_to_file")
 
 
+class Pool:
+    """Device memory pool over HIP virtual memory (see gms_pool_* in include/gms.h)."""
+
+    def __init__(self, va_bytes: int, slab_bytes: int = 0, device: int = 0):
+        h = VP()
+        _check(_pool_create(device, va_bytes, slab_bytes, ctypes.byref(h)), "gms_pool_create")
+        self._h = h
+        self.device = device
+
+    def close(self) -> None:
+        if getattr(self, "_h", None) is not None and self._h.value:
+            _pool_destroy(self._h)
+            self._h = VP()
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    def alloc(self, nbytes: int, align: int = 0) -> int:
+        out = U64()
+        _check(_pool_alloc(self._h, nbytes, align, ctypes.byref(out)), "gms_pool_alloc")
+        return int(out.value)
+
+    def free(self, addr: int) -> None:
+        _check(_pool_free(self._h, addr), "gms_pool_free")
+
+    def release(self, addr: int, nbytes: int) -> None:
+        _check(_pool_release(self._h, addr, nbytes), "gms_pool_release")
+
+    def remap(self, addr: int, nbytes: int) -> None:
+        _check(_pool_remap(self._h, addr, nbytes), "gms_pool_remap")
+
+    def set_access(self, addr: int, nbytes: int, read_only: bool) -> None:
+        _check(_pool_set_access(self._h, addr, nbytes, 1 if read_only else 0), "gms_pool_set_access")
+
+    def info(self) -> dict:
+        v = [U64() for _ in range(5)]
+        _check(_pool_info(self._h, *[ctypes.byref(x) for x in v]), "gms_pool_info")
+        return dict(zip(["base", "reserved", "mapped_bytes", "mappings", "granularity"], [int(x.value) for x in v]))
+
+    def mapping_of(self, addr: int):
+        a, b, m = U64(), U64(), INT()
+        _check(_pool_mapping_of(self._h, addr, ctypes.byref(a), ctypes.byref(b), ctypes.byref(m)),
+               "gms_pool_mapping_of")
+        return int(a.value), int(b.value), bool(m.value)
+
+
 def status_str(rc: int) -> str:
     return _status_str(rc).decode()
 
@@ -236,6 +294,8 @@ gms_restore = _restore
 gms_verify = _verify
 gms_layout = _layout
 gms_restore_from_file = _restore_file
+gms_pool_create = _pool_create
+gms_pool_alloc = _pool_alloc
 gms_snapshot_to_file = _snapshot_file
 gms_manifest_set_staging = _set_staging
 gms_status_str = _status_str
