@@ -159,7 +159,8 @@ int check_device_range(const void *ptr, uint64_t bytes, int device, const char *
     return GMS_OK;
 }
 
-int check_pinned(const void *ptr, const char *what)
+// [ptr, ptr + bytes) must lie inside one pinned host allocation.
+int check_pinned(const void *ptr, uint64_t bytes, const char *what)
 {
     if (!ptr) return fail(GMS_ERR_INVALID, "%s: null pointer", what);
     hipPointerAttribute_t attr;
@@ -168,6 +169,17 @@ int check_pinned(const void *ptr, const char *what)
         (void)hipGetLastError();
         return fail(GMS_ERR_INVALID, "%s: %p is not pinned host memory", what, ptr);
     }
+    hipDeviceptr_t base = nullptr;
+    size_t size = 0;
+    e = hipMemGetAddressRange(&base, &size, (hipDeviceptr_t)ptr);
+    if (e != hipSuccess) {
+        (void)hipGetLastError();
+        return fail(GMS_ERR_INVALID, "%s: no pinned allocation contains %p", what, ptr);
+    }
+    const uint64_t lo = (uint64_t)(uintptr_t)ptr, b = (uint64_t)(uintptr_t)base;
+    if (lo + bytes > b + size)
+        return fail(GMS_ERR_SIZE, "%s: %llu bytes at %p run past the end of its pinned allocation", what,
+                    (unsigned long long)bytes, ptr);
     return GMS_OK;
 }
 
@@ -184,7 +196,7 @@ int check_common(const gms_manifest *m, const void *image, uint64_t image_bytes,
     if (m->image_bytes == 0) return GMS_OK;
     if (((uintptr_t)image & 15) != 0) return fail(GMS_ERR_INVALID, "image %p is not 16-byte aligned", image);
     if (kind == GMS_MEM_DEVICE) return check_device_range(image, m->image_bytes, m->device, "image");
-    return check_pinned(image, "image");
+    return check_pinned(image, m->image_bytes, "image");
 }
 
 int check_outputs(const gms_manifest *m, const HashOut &h)

@@ -306,20 +306,26 @@ constexpr uint64_t kMaxGrid = 1u << 20;
 // (read-only) only needs the wave partials and runs at full occupancy.
 constexpr size_t kLdsCopy = 96 * 1024;
 constexpr size_t kLdsVerify = kWaves * sizeof(uint64_t);
+constexpr int kMaxDevices = 64;
 
 template <int OP, bool HASH>
 hipError_t launch_t(const Chunk *chunks, uint64_t first, uint64_t count, uint8_t *img_base,
                     uint64_t img_origin, const HashOut &h, hipStream_t s)
 {
     constexpr size_t lds = OP == kVerify ? kLdsVerify : kLdsCopy;
-    static std::once_flag attr_once;
-    static hipError_t attr_err = hipSuccess;
-    std::call_once(attr_once, [] {
-        if (lds > 64 * 1024)
-            attr_err = hipFuncSetAttribute((const void *)k_stream<OP, HASH>,
-                                           hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
-    });
-    if (attr_err != hipSuccess) return attr_err;
+    if (lds > 64 * 1024) {  // opt in to more than 64 KiB of dynamic LDS, once per device
+        static std::once_flag attr_once[kMaxDevices];
+        static hipError_t attr_err[kMaxDevices];
+        int dev = 0;
+        hipError_t e = hipGetDevice(&dev);
+        if (e != hipSuccess) return e;
+        if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+        std::call_once(attr_once[dev], [dev] {
+            attr_err[dev] = hipFuncSetAttribute((const void *)k_stream<OP, HASH>,
+                                                hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+        });
+        if (attr_err[dev] != hipSuccess) return attr_err[dev];
+    }
     const uint64_t grid = count < kMaxGrid ? count : kMaxGrid;
     hipLaunchKernelGGL((k_stream<OP, HASH>), dim3((uint32_t)grid), dim3(kThreads), lds, s, chunks + first, count,
                        (gbyte *)img_base, img_origin, h);

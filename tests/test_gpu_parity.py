@@ -265,6 +265,15 @@ def test_argument_errors_on_gpu():
         gms.Manifest([(raw.value + 100, (1 << 20) - 100)], device=0).close()
     finally:
         hip.hipFree(raw)
+    # a pinned image smaller than the size the caller claims
+    small_pinned = ctypes.c_void_p()
+    assert hip.hipHostMalloc(ctypes.byref(small_pinned), ctypes.c_size_t(m.image_bytes - 4096), 0) == 0
+    try:
+        with pytest.raises(gms.GmsError) as e:
+            gms.restore(m, small_pinned.value, m.image_bytes, gms.MEM_HOST_PINNED)
+        assert e.value.status == gms.GMS_ERR_SIZE
+    finally:
+        hip.hipHostFree(small_pinned)
     with pytest.raises(gms.GmsError) as e:  # host memory as an entry
         gms.Manifest([(host.ctypes.data, 100)], device=0)
     assert e.value.status == gms.GMS_ERR_INVALID
