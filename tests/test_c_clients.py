@@ -75,3 +75,28 @@ int main(void) {
     assert r.returncode == 0, r.stderr
     r = _run([str(exe)])
     assert r.returncode == 0 and "oracle sanitized ok" in r.stdout, r.stdout + r.stderr
+
+
+def test_host_code_under_sanitizers(tmp_path):
+    """The library's host code (validation, overlap sort, layout, chunking) under ASan/UBSan."""
+    lib = tmp_path / "libgms_san.so"
+    srcs = sorted(os.path.join(ROOT, "paper_2609_25451_amd", "csrc", f)
+                  for f in os.listdir(os.path.join(ROOT, "paper_2609_25451_amd", "csrc")) if f.endswith(".hip"))
+    hipcc = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
+    r = _run([hipcc, "--offload-arch=gfx950", "-O1", "-g", "-std=c++17", "-fPIC", "-shared",
+              "-Xarch_host", "-fsanitize=address", "-Xarch_host", "-fsanitize=undefined",
+              "-Xarch_host", "-fno-omit-frame-pointer", "-I", os.path.join(ROOT, "include"), *srcs, "-o", str(lib)])
+    assert r.returncode == 0, r.stderr[-2000:]
+    exe = tmp_path / "fuzz"
+    clang = os.path.join(os.path.dirname(os.path.realpath(hipcc)), "..", "lib", "llvm", "bin", "clang")
+    if not os.path.exists(clang):
+        clang = "/opt/rocm/llvm/bin/clang"
+    # the sanitized library carries clang's sanitizer runtime, so the driver is linked by clang too
+    r = _run([clang, "-std=c99", "-O1", "-g", "-fsanitize=address,undefined", "-I", os.path.join(ROOT, "include"),
+              os.path.join(HERE, "c", "manifest_fuzz.c"), str(lib), f"-Wl,-rpath,{tmp_path}", "-o", str(exe)])
+    if r.returncode != 0 and "asan" in r.stderr.lower():
+        pytest.skip("sanitizer runtime not available: " + r.stderr[:200])
+    assert r.returncode == 0, r.stderr[-2000:]
+    env = dict(os.environ, ASAN_OPTIONS="detect_leaks=0", UBSAN_OPTIONS="halt_on_error=1")
+    r = _run([str(exe)], env=env)
+    assert r.returncode == 0 and "manifest fuzz ok" in r.stdout, (r.stdout + r.stderr)[-3000:]
