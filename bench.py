@@ -29,7 +29,7 @@ sys.path.insert(0, ROOT)
 
 METRIC = "restore+verify GB/s on 1 GPU; seconds to restore a 16 GB weight shard"
 HBM_PEAK_GBS = 8000.0
-ALL_ROWS = ["main", "snapshot", "plain", "verify", "h2d", "file", "kv", "kv_vmm", "copy", "cpu"]
+ALL_ROWS = ["main", "snapshot", "plain", "verify", "h2d", "file", "kv", "kv_vmm", "copy", "cpu", "shards"]
 KERNEL_SOURCES = ["paper_2609_25451_amd/csrc/gms_kernels.hip", "paper_2609_25451_amd/csrc/gms_internal.h"]
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_restore_verify_llama8b.json")
 
@@ -263,6 +263,13 @@ def main():
     if "cpu" in rows:
         cpu = bench_cpu(torch, np, image, m, specs)
 
+    if "shards" in rows:  # last: frees the llama8b buffers to make room for the 122 GB MoE shard
+        del tensors, image, expected, ten_hash, cnt, mlist
+        m.close()
+        torch.cuda.synchronize()
+        torch.cuda.empty_cache()
+        result_rows["shards"] = {name: bench_shard(torch, gms, synth, timer, name) for name in ("llama70b_tp8", "moe")}
+
     value = P * args.steps / wall / 1e9 if main_times else None
     out = {
         "metric": METRIC,
@@ -402,6 +409,32 @@ def bench_kv(torch, np, gms, synth, timer):
     return {"entries": m.num_entries, "payload_bytes": P, "s": t, "GB_s": P / t / 1e9,
             "hbm_frac": 2 * P / t / 1e9 / HBM_PEAK_GBS, "mismatches": c, "flagged": flagged,
             "planted_block": int(base[e] + blk), "dead_units_untouched_first4_layers": dead_ok}
+
+
+def bench_shard(torch, gms, synth, timer, name):
+    """Fused restore+verify of another weight workload from a device-resident image."""
+    _, specs = synth.weight_set(name)
+    P = sum(sp.nbytes for sp in specs)
+    free, _ = torch.cuda.mem_get_info()
+    if free < 2 * P + (4 << 30):
+        return {"skipped": f"needs {2 * P} bytes of device memory, {free} free"}
+    seed, specs, tensors = build_weights(torch, synth, name)
+    m = gms.Manifest(tensors, device=0)
+    img = torch.empty(m.image_bytes, dtype=torch.uint8, device="cuda")
+    exp = torch.zeros(m.num_blocks, dtype=torch.int64, device="cuda")
+    gms.snapshot(m, img, m.image_bytes, blk_hash=exp)
+    cnt = torch.zeros(1, dtype=torch.int64, device="cuda")
+    ts = timer.run(lambda: gms.restore(m, img, m.image_bytes, expected=exp, mismatch_count=cnt), 5)
+    assert int(cnt.item()) == 0
+    t = statistics.median(ts)
+    out = {"tensors": len(tensors), "payload_bytes": P, "chunks": m.num_chunks, "restore_verify_s": t,
+           "restore_verify_GB_s": P / t / 1e9, "hbm_frac": (2 * P + 8 * m.num_blocks) / t / 1e9 / HBM_PEAK_GBS}
+    log(f"{name}: restore+verify {t * 1e3:.2f} ms, {out['hbm_frac'] * 100:.1f}% of HBM peak")
+    m.close()
+    del tensors, img, exp
+    torch.cuda.synchronize()
+    torch.cuda.empty_cache()
+    return out
 
 
 def bench_kv_vmm(torch, np, gms, synth, timer):
