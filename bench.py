@@ -113,13 +113,13 @@ def main():
     t0 = time.time()
     seed, specs, tensors = build_weights(torch, synth, "llama8b")
     m = gms.Manifest(tensors, device=0)
-    P, nb, n = m.payload_bytes, m.num_blocks, m.num_entries
+    P, nb, n, nchunks = m.payload_bytes, m.num_blocks, m.num_entries, m.num_chunks
     image = torch.empty(m.image_bytes, dtype=torch.uint8, device="cuda")
     expected = torch.zeros(nb, dtype=torch.int64, device="cuda")
     ten_hash = torch.zeros(n, dtype=torch.int64, device="cuda")
     gms.snapshot(m, image, m.image_bytes, gms.MEM_DEVICE, blk_hash=expected, ten_hash=ten_hash)
     torch.cuda.synchronize()
-    log(f"llama8b: {n} tensors, {P} B, {nb} blocks, {m.num_chunks} chunks; setup {time.time() - t0:.1f}s")
+    log(f"llama8b: {n} tensors, {P} B, {nb} blocks, {nchunks} chunks; setup {time.time() - t0:.1f}s")
 
     cnt = torch.zeros(1, dtype=torch.int64, device="cuda")
     mlist = torch.zeros(64, dtype=torch.int64, device="cuda")
@@ -287,7 +287,7 @@ def main():
         "config": {
             "workload": "llama8b bf16 weight set: 32 layers, d_model 4096, GQA 32q/8kv x 128, SwiGLU ffn 14336, "
                         "vocab 128256; 291 tensors; device-resident image; fused restore+verify",
-            "payload_bytes": P, "entries": n, "blocks": nb, "chunks": m.num_chunks, "block_bytes": 4096,
+            "payload_bytes": P, "entries": n, "blocks": nb, "chunks": nchunks, "block_bytes": 4096,
         },
         "seconds_to_restore_16GB": {
             "device_image_restore_verify": round(statistics.mean(main_times), 6) if main_times else None,

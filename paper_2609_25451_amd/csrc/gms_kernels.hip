@@ -39,6 +39,7 @@ constexpr uint64_t kSegStrideG = 128ull * kG;    // word-index step between a la
 constexpr uint64_t kBlockStrideG = 512ull * kG;  // word-index step between blocks
 constexpr int kWaves = kThreads / 64;            // waves per workgroup
 constexpr int kDepth = 2;                        // blocks each wave keeps loading ahead
+constexpr uint32_t kXcds = 8;                    // accelerator complex dies on MI355X
 
 __device__ __forceinline__ uint64_t mix64(uint64_t z)
 {
@@ -192,7 +193,15 @@ k_stream(const Chunk *__restrict__ chunks, uint64_t count, gbyte *__restrict__ i
     const bool check = HASH && h.expected != nullptr;
     const uint64_t *const exp_dummy = (const uint64_t *)chunks;  // any readable word
 
-    for (uint64_t ci = blockIdx.x; ci < count; ci += gridDim.x) {
+    // XCD-aware order: the dispatcher hands workgroup IDs to the 8 XCDs round
+    // robin, so within each grid-sized round, XCD x takes the x-th contiguous
+    // eighth of the chunks and every XCD streams its own contiguous region of
+    // the image and of the entries.
+    const uint64_t per_xcd = gridDim.x / kXcds;  // the grid is a multiple of kXcds
+    const uint64_t slot_in_round = (blockIdx.x % kXcds) * per_xcd + blockIdx.x / kXcds;
+    for (uint64_t round = 0; round < count; round += gridDim.x) {
+        const uint64_t ci = round + slot_in_round;
+        if (ci >= count) break;
         const Chunk c = chunks[ci];
         const uint32_t nblk = (c.len + kBlockBytes - 1) / kBlockBytes;
         const uint32_t nfull = fast_blocks(c);
@@ -300,7 +309,7 @@ k_prologue(uint64_t *__restrict__ ten, uint64_t n, uint64_t *__restrict__ mm_cou
     if (mm_count && tid == 0) *mm_count = 0;
 }
 
-constexpr uint64_t kMaxGrid = 1u << 20;
+constexpr uint64_t kMaxGrid = 1u << 20;  // a multiple of kXcds
 // Dynamic LDS per workgroup: restore and snapshot ask for more than half of a
 // CU's 160 KiB so that one 8-wave workgroup is resident per CU; verify
 // (read-only) only needs the wave partials and runs at full occupancy.
@@ -326,7 +335,7 @@ hipError_t launch_t(const Chunk *chunks, uint64_t first, uint64_t count, uint8_t
         });
         if (attr_err[dev] != hipSuccess) return attr_err[dev];
     }
-    const uint64_t grid = count < kMaxGrid ? count : kMaxGrid;
+    const uint64_t grid = ((count < kMaxGrid ? count : kMaxGrid) + kXcds - 1) / kXcds * kXcds;
     hipLaunchKernelGGL((k_stream<OP, HASH>), dim3((uint32_t)grid), dim3(kThreads), lds, s, chunks + first, count,
                        (gbyte *)img_base, img_origin, h);
     return hipGetLastError();
