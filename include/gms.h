@@ -79,7 +79,7 @@ extern "C" {
 #endif
 
 #define GMS_BLOCK_BYTES 4096u
-#define GMS_DEFAULT_CHUNK_BYTES (256u * 1024u)
+#define GMS_DEFAULT_CHUNK_BYTES (64u * 1024u)
 #define GMS_HOST_ONLY (-1)
 
 /* One device address range of engine state: [addr, addr + nbytes). */

@@ -64,7 +64,7 @@ def test_workload_layouts(name):
     m = _host_manifest(sizes)
     _, _, ib, nb = oracle.layout(sizes)
     assert m.image_bytes == ib and m.num_blocks == nb
-    assert m.num_chunks == _expected_chunks(sizes, 256 * 1024)
+    assert m.num_chunks == _expected_chunks(sizes, 64 * 1024)
     m4 = _host_manifest(sizes, chunk_bytes=1 << 20)
     assert m4.num_chunks == _expected_chunks(sizes, 1 << 20)
 
