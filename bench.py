@@ -30,7 +30,9 @@ sys.path.insert(0, ROOT)
 METRIC = "restore+verify GB/s on 1 GPU; seconds to restore a 16 GB weight shard"
 HBM_PEAK_GBS = 8000.0
 ALL_ROWS = ["main", "snapshot", "plain", "verify", "h2d", "file", "kv", "kv_vmm", "copy", "cpu", "shards"]
-KERNEL_SOURCES = ["paper_2609_25451_amd/csrc/gms_kernels.hip", "paper_2609_25451_amd/csrc/gms_internal.h"]
+# The kernel, its launch configuration and the chunking that shapes its accesses.
+KERNEL_SOURCES = ["paper_2609_25451_amd/csrc/gms_kernels.hip", "paper_2609_25451_amd/csrc/gms_internal.h",
+                  "paper_2609_25451_amd/csrc/gms_api.hip", "include/gms.h"]
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_restore_verify_llama8b.json")
 
 
