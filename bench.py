@@ -320,18 +320,29 @@ def bench_file(torch, gms, m, expected):
         gms.snapshot_to_file(m, path, flags=gms.FILE_DIRECT | gms.FILE_SYNC)
         torch.cuda.synchronize()
         out["snapshot_direct_sync_s"] = time.perf_counter() - t0
-        out["storage_read_direct_GB_s"] = raw_direct_read(path, m.image_bytes) / 1e9
-        for label, flags in (("restore_verify_direct", gms.FILE_DIRECT), ("restore_verify_buffered_cold", 0),
-                             ("restore_verify_buffered_cached", 0)):
+        def restore(flags):
             torch.cuda.synchronize()
             t0 = time.perf_counter()
             gms.restore_from_file(m, path, flags=flags, expected=expected, mismatch_count=cnt)
             torch.cuda.synchronize()
             t = time.perf_counter() - t0
-            assert int(cnt.item()) == 0, f"{label}: mismatches"
-            out[label + "_s"] = t
-            out[label + "_GB_s"] = m.payload_bytes / t / 1e9
-        out["storage_frac"] = out["restore_verify_direct_GB_s"] / out["storage_read_direct_GB_s"]
+            assert int(cnt.item()) == 0, "file restore reported mismatches"
+            return m.payload_bytes / t / 1e9
+
+        # The shared disk's speed drifts within a run (it is slow right after the write), so raw
+        # O_DIRECT reads and direct restores alternate and the best of each is compared.
+        raw, direct = [], []
+        for _ in range(3):
+            raw.append(raw_direct_read(path, m.image_bytes) / 1e9)
+            direct.append(restore(gms.FILE_DIRECT))
+        cold = restore(0)    # buffered; O_DIRECT reads left the page cache cold
+        cached = restore(0)  # buffered, now from the page cache
+        out.update({
+            "restore_verify_direct_GB_s": max(direct), "restore_verify_direct_s": m.payload_bytes / max(direct) / 1e9,
+            "restore_verify_direct_runs_GB_s": direct, "storage_read_direct_GB_s": max(raw),
+            "storage_read_direct_runs_GB_s": raw, "storage_frac": max(direct) / max(raw),
+            "restore_verify_buffered_cold_GB_s": cold, "restore_verify_buffered_cached_GB_s": cached,
+        })
         log(f"file restore+verify: direct {out['restore_verify_direct_GB_s']:.1f} GB/s "
             f"(raw direct read {out['storage_read_direct_GB_s']:.1f} GB/s), "
             f"cached {out['restore_verify_buffered_cached_GB_s']:.1f} GB/s")
@@ -341,25 +352,24 @@ def bench_file(torch, gms, m, expected):
     return out
 
 
-def raw_direct_read(path, nbytes, threads=8, piece=16 << 20):
-    """Bytes/s of plain parallel O_DIRECT reads of the file (the storage side alone)."""
+def raw_direct_read(path, nbytes, threads=16, piece=16 << 20):
+    """Bytes/s of plain parallel O_DIRECT reads of the file (the storage side alone), in the
+    library's own request shape: `threads` workers taking `piece`-byte reads in file order."""
     import mmap
     import threading
 
     fd = os.open(path, os.O_RDONLY | getattr(os, "O_DIRECT", 0))
     try:
-        per = -(-nbytes // threads)
-        per = -(-per // piece) * piece
+        npieces = -(-nbytes // piece)
 
         def work(t):
             buf = mmap.mmap(-1, piece)
-            lo, hi = t * per, min(nbytes, (t + 1) * per)
-            p = lo
-            while p < hi:
-                n = os.preadv(fd, [memoryview(buf)[: min(piece, hi - p)]], p)
-                if n <= 0:
+            for i in range(t, npieces, threads):
+                lo = i * piece
+                want = min(piece, nbytes - lo)
+                n = os.preadv(fd, [memoryview(buf)[:want]], lo)
+                if n != want:
                     raise OSError("short read")
-                p += n
             buf.close()
 
         t0 = time.perf_counter()

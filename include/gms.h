@@ -205,12 +205,14 @@ enum gms_file_flags {
  * replacement's model state is re-read from storage while its runtime is
  * restored; section 3.1: the transfer costs S / B_eff).  The file holds the
  * packed image (the layout above, no header) starting at `file_offset`.
- * Each 64 MiB slice is read with `io_threads` parallel preads (0 = 8) into a
- * pinned host slot, DMA'd into a device slot on the manifest's copy stream and
- * scattered (and hashed / compared, as gms_restore) by the kernel on `stream`;
- * a host slot is refilled once its DMA has finished.  The call returns when
- * every slice has been read and enqueued; device work completes on `stream`.
- * The first call allocates the manifest's pinned host ring (slots x slice).
+ * `io_threads` workers (0 = 16) read the image in pieces (16 MiB with
+ * O_DIRECT, 64 MiB or one slice buffered), in file order, into the slices of
+ * a pinned host ring; each full slice is DMA'd into
+ * a device slot on the manifest's copy stream and scattered (and hashed /
+ * compared, as gms_restore) by the kernel on `stream`; a host slot is refilled
+ * once its DMA has finished.  The call returns when every slice has been read
+ * and enqueued; device work completes on `stream`.  The first file call
+ * allocates the manifest's pinned host ring: 2 x slots (at most 16) slices.
  * Errors: as gms_restore, plus GMS_ERR_IO (open/read failure) and
  * GMS_ERR_SIZE (file shorter than file_offset + gms_image_bytes).
  */
@@ -220,8 +222,9 @@ int gms_restore_from_file(const gms_manifest *m, const char *path, uint64_t file
                           uint64_t mismatch_cap, void *stream);
 
 /*
- * Writes the packed image to `path` (created or truncated), gathering on the
- * device and draining the ring to the file with pwrite; optionally emits the
+ * Writes the packed image to `path` (created or truncated): the kernel gathers
+ * each slice into a slot of the pinned host ring and `io_threads` workers
+ * (0 = 16) write its 16 MiB pieces with pwrite; optionally emits the
  * block / tensor hashes of the gathered bytes.  Synchronous: the file is
  * complete when the call returns (durable too with GMS_FILE_SYNC).
  * Errors: GMS_ERR_STATE, GMS_ERR_INVALID, GMS_ERR_IO, GMS_ERR_HIP, GMS_ERR_NOMEM.

@@ -59,6 +59,7 @@ void free_ring(gms_manifest *m)
     }
     if (m->h_ring) (void)hipHostFree(m->h_ring);
     m->h_ring = nullptr;
+    m->host_slots = 0;
     if (m->ev_entry) (void)hipEventDestroy(m->ev_entry);
     if (m->ev_done) (void)hipEventDestroy(m->ev_done);
     if (m->copy_stream) (void)hipStreamDestroy(m->copy_stream);
@@ -96,8 +97,7 @@ int ensure_ring(gms_manifest *m)
         return free_ring(m), fail_hip(e, "staging ring: hipStreamCreate");
     for (uint32_t i = 0; i < m->slots; ++i) {
         if ((e = hipEventCreateWithFlags(&m->ev_filled[i], hipEventDisableTiming)) != hipSuccess ||
-            (e = hipEventCreateWithFlags(&m->ev_free[i], hipEventDisableTiming)) != hipSuccess ||
-            (e = hipEventCreateWithFlags(&m->ev_host[i], hipEventDisableTiming)) != hipSuccess)
+            (e = hipEventCreateWithFlags(&m->ev_free[i], hipEventDisableTiming)) != hipSuccess)
             return free_ring(m), fail_hip(e, "staging ring: hipEventCreate");
     }
     if ((e = hipEventCreateWithFlags(&m->ev_entry, hipEventDisableTiming)) != hipSuccess ||
@@ -122,13 +122,22 @@ int ensure_host_ring(gms_manifest *m)
     if (rc != GMS_OK) return rc;
     if (!m->d_ring) return fail(GMS_ERR_STATE, "file paths need the staging ring (slots > 0)");
     if (m->h_ring) return GMS_OK;
-    hipError_t e = hipHostMalloc((void **)&m->h_ring, m->ring_slice * m->ring_slots, hipHostMallocDefault);
+    const uint32_t hk = std::min<uint32_t>(kMaxSlots, 2 * m->ring_slots);
+    hipError_t e = hipHostMalloc((void **)&m->h_ring, m->ring_slice * hk, hipHostMallocDefault);
     if (e != hipSuccess) {
         m->h_ring = nullptr;
         (void)hipGetLastError();
         return fail(GMS_ERR_NOMEM, "pinned host ring: hipHostMalloc(%llu) failed: %s",
-                    (unsigned long long)(m->ring_slice * m->ring_slots), hipGetErrorString(e));
+                    (unsigned long long)(m->ring_slice * hk), hipGetErrorString(e));
     }
+    for (uint32_t i = 0; i < hk; ++i)
+        if ((e = hipEventCreateWithFlags(&m->ev_host[i], hipEventDisableTiming)) != hipSuccess) {
+            for (uint32_t j = 0; j < i; ++j) (void)hipEventDestroy(m->ev_host[j]), m->ev_host[j] = nullptr;
+            (void)hipHostFree(m->h_ring);
+            m->h_ring = nullptr;
+            return fail_hip(e, "pinned host ring: hipEventCreate");
+        }
+    m->host_slots = hk;
     return GMS_OK;
 }
 

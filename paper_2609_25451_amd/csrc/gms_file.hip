@@ -7,10 +7,13 @@
 // parallel pread (O_DIRECT through per-worker bounce buffers when the file
 // system allows it, buffered otherwise) into a pinned host slot, a DMA of
 // that slot into a device slot on the manifest's copy stream, and the
-// scatter(+hash) kernel on the caller's stream.  Host slots are reused
-// once the DMA that read them has finished, so storage, the host link and HBM
-// all stay busy.  Snapshot gathers each slice straight into a pinned host slot
-// (zero-copy) and writes it with pwrite.
+// scatter(+hash) kernel on the caller's stream.  One pool of I/O workers
+// takes pieces (16 MiB direct, up to 64 MiB buffered) in file order from a
+// shared counter, so every worker keeps a large request in flight and none
+// waits for a slower slice; a host slot is refilled once the DMA that read it
+// has finished, so storage, the host link and HBM all stay busy.  Snapshot runs the mirror image: the
+// gather kernel writes each slice straight into a pinned host slot (zero-copy)
+// and the workers write its pieces to the file.
 
 #include <fcntl.h>
 #include <sys/stat.h>
@@ -19,9 +22,9 @@
 #include <algorithm>
 #include <atomic>
 #include <cerrno>
+#include <condition_variable>
 #include <cstdlib>
 #include <cstring>
-#include <future>
 #include <mutex>
 #include <thread>
 #include <vector>
@@ -36,9 +39,14 @@ using gms::HashOut;
 
 namespace {
 
-constexpr unsigned kDefaultIoThreads = 8;
+constexpr unsigned kDefaultIoThreads = 16;
 constexpr unsigned kMaxIoThreads = 64;
 constexpr uint64_t kDirectAlign = 4096;
+// One pread/pwrite.  Direct I/O loses storage bandwidth below 16 MiB per
+// request; buffered reads go through the page cache's readahead and copy,
+// which run best at 64 MiB per request (at most one slice).
+constexpr uint64_t kDirectPieceBytes = 16ull << 20;
+constexpr uint64_t kBufferedPieceBytes = 64ull << 20;
 
 struct FileHandle {
     int fd = -1;
@@ -49,85 +57,167 @@ struct FileHandle {
     }
 };
 
-// Per-call I/O context: `lanes` independent transfers (one per ring slot in
-// flight) of `threads` workers each.  Direct I/O cannot target the pinned
-// slots (the kernel refuses to pin driver-mapped pages: EFAULT), so with
-// O_DIRECT every worker moves data through a private page-aligned bounce
-// buffer and copies to or from the pinned slot; buffered I/O reads and writes
-// the slot itself.
-struct IoCtx {
-    int fd = -1;
-    bool direct = false;
-    unsigned threads = 1;
-    uint64_t bounce_bytes = 0;
-    std::vector<uint8_t *> bounce;  // [lane * threads + worker]
-    ~IoCtx()
-    {
-        for (uint8_t *b : bounce) free(b);
-    }
-    int init(int fd_, bool direct_, unsigned lanes, unsigned threads_, uint64_t slice)
-    {
-        fd = fd_;
-        direct = direct_;
-        threads = threads_;
-        if (!direct) return GMS_OK;
-        bounce_bytes = std::min<uint64_t>(16ull << 20, ceil_div(ceil_div(slice, threads), kDirectAlign) * kDirectAlign);
-        for (unsigned t = 0; t < lanes * threads; ++t) {
-            void *b = nullptr;
-            if (posix_memalign(&b, kDirectAlign, bounce_bytes) != 0) return fail(GMS_ERR_NOMEM, "bounce buffer");
-            bounce.push_back((uint8_t *)b);
-        }
-        return GMS_OK;
-    }
-};
-
-// One worker's share: bytes [lo, hi) of buf <-> file offset off + lo, using
-// bounce buffer `b` for direct I/O.  Returns 0 or an errno value (EIO for a
-// file that ends early).
-int transfer_range(const IoCtx &io, uint8_t *b, uint8_t *buf, uint64_t lo, uint64_t hi, uint64_t off, bool write,
-                   const std::atomic<int> &stop)
+// Moves `len` bytes between `buf` and file offset `off`.  Direct I/O cannot
+// target the pinned slots (the kernel refuses to pin driver-mapped pages:
+// EFAULT), so with O_DIRECT the bytes go through the worker's page-aligned
+// bounce buffer.  Returns 0 or an errno value (EIO for a file that ends early).
+int transfer_piece(int fd, uint8_t *bounce, uint8_t *buf, uint64_t len, uint64_t off, bool write)
 {
-    uint64_t p = lo;
-    while (p < hi && !stop.load(std::memory_order_relaxed)) {
-        const uint64_t want = io.direct ? std::min(hi - p, io.bounce_bytes) : hi - p;
-        uint8_t *mem = io.direct ? b : buf + p;
-        if (write && io.direct) memcpy(mem, buf + p, want);
-        uint64_t done = 0;
-        while (done < want) {
-            ssize_t r = write ? pwrite(io.fd, mem + done, want - done, (off_t)(off + p + done))
-                              : pread(io.fd, mem + done, want - done, (off_t)(off + p + done));
-            if (r < 0) {
-                if (errno == EINTR) continue;
-                return errno;
-            }
-            if (r == 0) return EIO;
-            done += (uint64_t)r;
+    uint8_t *mem = bounce ? bounce : buf;
+    if (write && bounce) memcpy(bounce, buf, len);
+    uint64_t done = 0;
+    while (done < len) {
+        ssize_t r = write ? pwrite(fd, mem + done, len - done, (off_t)(off + done))
+                          : pread(fd, mem + done, len - done, (off_t)(off + done));
+        if (r < 0) {
+            if (errno == EINTR) continue;
+            return errno;
         }
-        if (!write && io.direct) memcpy(buf + p, mem, want);
-        p += want;
+        if (r == 0) return EIO;
+        done += (uint64_t)r;
     }
+    if (!write && bounce) memcpy(buf, bounce, len);
     return 0;
 }
 
-// Moves exactly `len` bytes between buf and file offset `off` with lane
-// `lane`'s workers on disjoint 4 KiB-aligned ranges.
-int transfer(const IoCtx &io, unsigned lane, uint8_t *buf, uint64_t len, uint64_t off, bool write)
-{
-    std::atomic<int> err{0};
-    uint64_t per = ceil_div(len, io.threads);
-    per = ceil_div(per, kDirectAlign) * kDirectAlign;
-    auto work = [&](unsigned t, uint64_t lo, uint64_t hi) {
-        uint8_t *b = io.direct ? io.bounce[lane * io.threads + t] : nullptr;
-        int e = transfer_range(io, b, buf, lo, hi, off, write, err);
-        if (e) err = e;
-    };
-    std::vector<std::thread> pool;
-    for (unsigned t = 1; t < io.threads && t * per < len; ++t)
-        pool.emplace_back(work, t, t * per, std::min(len, (t + 1) * per));
-    work(0, 0, std::min(len, per));
-    for (auto &t : pool) t.join();
-    return err.load();
-}
+// The image cut into slices (one host slot each) and each slice into pieces of
+// at most `piece` bytes, numbered in file order.  `enqueued` counts the slices
+// whose device-side step the caller's thread has enqueued; `left[s]` counts
+// the pieces of slice s not yet transferred.  The first error stops every
+// worker.
+struct PiecePool {
+    uint64_t slice = 0, image_bytes = 0, piece = 0, per_slice = 0, nslices = 0, npieces = 0;
+    uint64_t file_offset = 0;  // file position of image byte 0
+    std::atomic<uint64_t> next{0};
+    std::mutex mu;
+    std::condition_variable cv;
+    std::vector<uint32_t> left;
+    uint64_t enqueued = 0;
+    int err = 0;        // errno of the first failed transfer
+    bool hip_err = false;
+    bool stop = false;
+
+    PiecePool(uint64_t slice_, uint64_t image_bytes_, uint64_t piece_)
+        : slice(slice_), image_bytes(image_bytes_), piece(std::min(piece_, slice_))
+    {
+        per_slice = ceil_div(slice, piece);
+        nslices = ceil_div(image_bytes, slice);
+        npieces = nslices * per_slice;
+        left.resize(nslices);
+        for (uint64_t s = 0; s < nslices; ++s)
+            left[s] = (uint32_t)ceil_div(std::min(slice, image_bytes - s * slice), piece);
+    }
+    // image range of piece p; empty for the padding pieces of a short last slice
+    void range(uint64_t p, uint64_t &s, uint64_t &lo, uint64_t &bytes) const
+    {
+        s = p / per_slice;
+        lo = s * slice + (p % per_slice) * piece;
+        const uint64_t end = std::min((s + 1) * slice, image_bytes);
+        bytes = lo < end ? std::min(piece, end - lo) : 0;
+    }
+    void fail_stop(int e, bool hip)
+    {
+        std::lock_guard<std::mutex> l(mu);
+        if (!err && !hip_err) {
+            err = e;
+            hip_err = hip;
+        }
+        stop = true;
+        cv.notify_all();
+    }
+    // blocks until `enqueued > s`; false once the pool has stopped
+    bool wait_enqueued(uint64_t s)
+    {
+        std::unique_lock<std::mutex> l(mu);
+        cv.wait(l, [&] { return stop || enqueued > s; });
+        return !stop;
+    }
+    void set_enqueued(uint64_t n)
+    {
+        std::lock_guard<std::mutex> l(mu);
+        enqueued = n;
+        cv.notify_all();
+    }
+    void piece_done(uint64_t s)
+    {
+        std::lock_guard<std::mutex> l(mu);
+        if (--left[s] == 0) cv.notify_all();
+    }
+    // blocks until every piece of slice s is done; false once the pool has stopped
+    bool wait_slice(uint64_t s)
+    {
+        std::unique_lock<std::mutex> l(mu);
+        cv.wait(l, [&] { return stop || left[s] == 0; });
+        return !stop;
+    }
+};
+
+// Runs `threads` workers over the pool.  A worker takes piece p of slice s in
+// host slot s % hslots; for a read it first waits until the DMA out of that
+// slot for slice s - hslots has been enqueued and has finished; for a write it
+// waits until the gather of slice s has been enqueued and has finished.
+class Workers {
+public:
+    Workers(PiecePool &pool, int fd, const char *path, bool direct, bool write, uint8_t *h_ring, uint32_t hslots,
+            const hipEvent_t *ev_host, unsigned threads)
+    {
+        for (unsigned t = 0; t < threads; ++t) {
+            try {
+                pool_.emplace_back([=, &pool] { run(pool, fd, path, direct, write, h_ring, hslots, ev_host); });
+            } catch (...) {  // no thread: stop the pool rather than wait for work nobody does
+                pool.fail_stop(EAGAIN, false);
+                break;
+            }
+        }
+    }
+    ~Workers() { join(); }
+    void join()
+    {
+        for (auto &t : pool_)
+            if (t.joinable()) t.join();
+    }
+
+private:
+    static void run(PiecePool &pool, int fd, const char *path, bool direct, bool write, uint8_t *h_ring,
+                    uint32_t hslots, const hipEvent_t *ev_host)
+    {
+        uint8_t *bounce = nullptr;
+        if (direct && posix_memalign((void **)&bounce, kDirectAlign, pool.piece) != 0) {
+            pool.fail_stop(ENOMEM, false);
+            return;
+        }
+        // Buffered reads: the kernel keeps readahead state per open file, and
+        // workers taking interleaved pieces through one descriptor defeat it,
+        // so each worker reads through a descriptor of its own (the shared
+        // one if the file cannot be opened again).
+        const int own = (!write && !direct && path) ? open(path, O_RDONLY | O_CLOEXEC) : -1;
+        for (;;) {
+            const uint64_t p = pool.next.fetch_add(1, std::memory_order_relaxed);
+            if (p >= pool.npieces) break;
+            uint64_t s, lo, bytes;
+            pool.range(p, s, lo, bytes);
+            if (bytes == 0) continue;
+            const uint32_t slot = (uint32_t)(s % hslots);
+            if (write || s >= hslots) {
+                if (!pool.wait_enqueued(write ? s : s - hslots)) break;
+                if (hipEventSynchronize(ev_host[slot]) != hipSuccess) {
+                    pool.fail_stop(0, true);
+                    break;
+                }
+            }
+            uint8_t *host = h_ring + (uint64_t)slot * pool.slice + (lo - s * pool.slice);
+            const int e = transfer_piece(own >= 0 ? own : fd, bounce, host, bytes, pool.file_offset + lo, write);
+            if (e) {
+                pool.fail_stop(e, false);
+                break;
+            }
+            pool.piece_done(s);
+        }
+        if (own >= 0) close(own);
+        free(bounce);
+    }
+    std::vector<std::thread> pool_;
+};
 
 int open_file(FileHandle &f, const char *path, bool write, bool want_direct, uint64_t offset)
 {
@@ -159,6 +249,17 @@ int drain_ring(gms_manifest *m)
     hipError_t e;
     if (m->copy_stream && (e = hipStreamSynchronize(m->copy_stream)) != hipSuccess) return fail_hip(e, "copy stream");
     if (m->done_recorded && (e = hipEventSynchronize(m->ev_done)) != hipSuccess) return fail_hip(e, "ring drain");
+    return GMS_OK;
+}
+
+// Stops and joins the workers, then reports the pool's first error (or `rc`).
+int finish(PiecePool &pool, Workers &w, int rc, const char *path, bool write)
+{
+    if (rc != GMS_OK) pool.fail_stop(0, false);
+    w.join();
+    if (rc != GMS_OK) return rc;
+    if (pool.hip_err) return fail(GMS_ERR_HIP, "waiting for a staging slot of %s", path);
+    if (pool.err) return fail(GMS_ERR_IO, "%s %s: %s", write ? "writing" : "reading", path, strerror(pool.err));
     return GMS_OK;
 }
 
@@ -204,60 +305,36 @@ int gms_restore_from_file(const gms_manifest *cm, const char *path, uint64_t fil
     if ((rc = gms::ensure_host_ring(m)) != GMS_OK) return rc;
     if ((rc = drain_ring(m)) != GMS_OK) return rc;
     const uint64_t slice = m->ring_slice;
-    const uint32_t k = m->ring_slots;
-    const uint64_t nslices = ceil_div(m->image_bytes, slice);
-    // every host slot has its own read in flight; the workers are shared out
-    const unsigned per_slot = std::max(1u, threads / k);
-    IoCtx io;
-    if ((rc = io.init(f.fd, f.direct, k, per_slot, slice)) != GMS_OK) return rc;
-    std::vector<std::future<int>> reads(k);
-    auto start_read = [&](uint64_t sl) -> int {
-        const uint32_t slot = (uint32_t)(sl % k);
-        if (sl >= k) GMS_TRY(hipEventSynchronize(m->ev_host[slot]));  // the DMA out of this slot is done
-        uint8_t *host = m->h_ring + (uint64_t)slot * slice;
-        const uint64_t lo = sl * slice;
-        const uint64_t bytes = std::min(slice, m->image_bytes - lo);
-        reads[slot] = std::async(std::launch::async, [&io, slot, host, bytes, lo, file_offset] {
-            return transfer(io, slot, host, bytes, file_offset + lo, false);
-        });
-        return GMS_OK;
-    };
-    // joins every read still in flight (they use `io` and the host slots)
-    auto join_reads = [&] {
-        for (auto &r : reads)
-            if (r.valid()) r.wait();
-    };
-
+    const uint32_t k = m->ring_slots, hk = m->host_slots;
     GMS_TRY(hipEventRecord(m->ev_entry, s));
     GMS_TRY(hipStreamWaitEvent(m->copy_stream, m->ev_entry, 0));
-    for (uint64_t sl = 0; sl < std::min<uint64_t>(k, nslices); ++sl)
-        if ((rc = start_read(sl)) != GMS_OK) return join_reads(), rc;
-    for (uint64_t sl = 0; sl < nslices; ++sl) {
-        const uint32_t slot = (uint32_t)(sl % k);
-        uint8_t *host = m->h_ring + (uint64_t)slot * slice;
+
+    PiecePool pool(slice, m->image_bytes, f.direct ? kDirectPieceBytes : kBufferedPieceBytes);
+    pool.file_offset = file_offset;
+    Workers w(pool, f.fd, path, f.direct, false, m->h_ring, hk, m->ev_host,
+              (unsigned)std::min<uint64_t>(threads, pool.npieces));
+    for (uint64_t sl = 0; sl < pool.nslices && rc == GMS_OK; ++sl) {
+        if (!pool.wait_slice(sl)) break;  // a worker failed
+        const uint32_t slot = (uint32_t)(sl % k), hslot = (uint32_t)(sl % hk);
+        uint8_t *host = m->h_ring + (uint64_t)hslot * slice;
         uint8_t *dev = m->d_ring + (uint64_t)slot * slice;
         const uint64_t lo = sl * slice;
         const uint64_t bytes = std::min(slice, m->image_bytes - lo);
-        const int err = reads[slot].get();
-        if (err) {
-            join_reads();
-            return fail(GMS_ERR_IO, "reading %s at %llu: %s", path, (unsigned long long)(file_offset + lo),
-                        strerror(err));
-        }
         hipError_t e;
         if ((sl >= k && (e = hipStreamWaitEvent(m->copy_stream, m->ev_free[slot], 0)) != hipSuccess) ||
             (e = hipMemcpyAsync(dev, host, bytes, hipMemcpyHostToDevice, m->copy_stream)) != hipSuccess ||
-            (e = hipEventRecord(m->ev_host[slot], m->copy_stream)) != hipSuccess ||
+            (e = hipEventRecord(m->ev_host[hslot], m->copy_stream)) != hipSuccess ||
             (e = hipEventRecord(m->ev_filled[slot], m->copy_stream)) != hipSuccess ||
             (e = hipStreamWaitEvent(s, m->ev_filled[slot], 0)) != hipSuccess ||
             (e = gms::launch_stream(gms::kRestore, h.any(), m->d_chunks, m->slice_first[sl],
                                     m->slice_first[sl + 1] - m->slice_first[sl], dev, lo, h, s)) != hipSuccess ||
             (e = hipEventRecord(m->ev_free[slot], s)) != hipSuccess) {
-            join_reads();
-            return fail_hip(e, "file restore slice");
+            rc = fail_hip(e, "file restore slice");
+            break;
         }
-        if (sl + k < nslices && (rc = start_read(sl + k)) != GMS_OK) return join_reads(), rc;
+        pool.set_enqueued(sl + 1);
     }
+    if ((rc = finish(pool, w, rc, path, false)) != GMS_OK) return rc;
     GMS_TRY(hipEventRecord(m->ev_done, s));
     m->done_recorded = true;
     return GMS_OK;
@@ -290,10 +367,7 @@ int gms_snapshot_to_file(const gms_manifest *cm, const char *path, uint32_t flag
     if ((rc = gms::ensure_host_ring(m)) != GMS_OK) return rc;
     if ((rc = drain_ring(m)) != GMS_OK) return rc;
     const uint64_t slice = m->ring_slice;
-    const uint32_t k = m->ring_slots;
-    const uint64_t nslices = ceil_div(m->image_bytes, slice);
-    IoCtx io;
-    if ((rc = io.init(f.fd, f.direct, 1, threads, slice)) != GMS_OK) return rc;
+    const uint32_t hk = m->host_slots;
     uint8_t *h_dev = nullptr;  // device view of the pinned host ring
     GMS_TRY(hipHostGetDevicePointer((void **)&h_dev, m->h_ring, 0));
 
@@ -301,25 +375,25 @@ int gms_snapshot_to_file(const gms_manifest *cm, const char *path, uint32_t flag
     // over the host link keep it saturated more steadily than a device slot
     // plus DMA)
     auto enqueue = [&](uint64_t sl) -> int {
-        const uint32_t slot = (uint32_t)(sl % k);
+        const uint32_t hslot = (uint32_t)(sl % hk);
         const uint64_t c0 = m->slice_first[sl], c1 = m->slice_first[sl + 1];
         GMS_TRY(gms::launch_stream(gms::kSnapshot, h.any(), m->d_chunks, c0, c1 - c0,
-                                   h_dev + (uint64_t)slot * slice, sl * slice, h, s));
-        GMS_TRY(hipEventRecord(m->ev_host[slot], s));
+                                   h_dev + (uint64_t)hslot * slice, sl * slice, h, s));
+        GMS_TRY(hipEventRecord(m->ev_host[hslot], s));
         return GMS_OK;
     };
 
-    for (uint64_t sl = 0; sl < std::min<uint64_t>(k, nslices); ++sl)
-        if ((rc = enqueue(sl)) != GMS_OK) return rc;
-    for (uint64_t sl = 0; sl < nslices; ++sl) {
-        const uint32_t slot = (uint32_t)(sl % k);
-        const uint64_t lo = sl * slice;
-        const uint64_t bytes = std::min(slice, m->image_bytes - lo);
-        GMS_TRY(hipEventSynchronize(m->ev_host[slot]));
-        int err = transfer(io, 0, m->h_ring + (uint64_t)slot * slice, bytes, lo, true);
-        if (err) return fail(GMS_ERR_IO, "writing %s at %llu: %s", path, (unsigned long long)lo, strerror(err));
-        if (sl + k < nslices && (rc = enqueue(sl + k)) != GMS_OK) return rc;
+    PiecePool pool(slice, m->image_bytes, kDirectPieceBytes);
+    Workers w(pool, f.fd, path, f.direct, true, m->h_ring, hk, m->ev_host,
+              (unsigned)std::min<uint64_t>(threads, pool.npieces));
+    const uint64_t first = std::min<uint64_t>(hk, pool.nslices);
+    for (uint64_t sl = 0; sl < first && rc == GMS_OK; ++sl) rc = enqueue(sl);
+    if (rc == GMS_OK) pool.set_enqueued(first);
+    for (uint64_t sl = 0; sl + hk < pool.nslices && rc == GMS_OK; ++sl) {
+        if (!pool.wait_slice(sl)) break;  // host slot sl % hk is written out: refill it
+        if ((rc = enqueue(sl + hk)) == GMS_OK) pool.set_enqueued(sl + hk + 1);
     }
+    if ((rc = finish(pool, w, rc, path, true)) != GMS_OK) return rc;
     GMS_TRY(hipEventRecord(m->ev_done, s));
     m->done_recorded = true;
     if ((flags & GMS_FILE_SYNC) && fsync(f.fd) != 0) return fail(GMS_ERR_IO, "fsync(%s): %s", path, strerror(errno));

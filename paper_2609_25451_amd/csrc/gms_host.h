@@ -61,7 +61,8 @@ struct gms_manifest {
     uint8_t *d_ring = nullptr;
     uint64_t ring_slice = 0;
     uint32_t ring_slots = 0;
-    uint8_t *h_ring = nullptr;  // pinned host slots (file paths only)
+    uint8_t *h_ring = nullptr;  // pinned host slots (file paths only), host_slots x ring_slice
+    uint32_t host_slots = 0;    // twice the device slots (capped), so reads run ahead of the DMAs
     hipStream_t copy_stream = nullptr;
     hipEvent_t ev_filled[gms::kMaxSlots] = {};
     hipEvent_t ev_free[gms::kMaxSlots] = {};

@@ -69,7 +69,11 @@ int set_access(gms_pool *p, uint64_t va, uint64_t bytes, bool read_only)
     acc.location = device_prop(p->device).location;
     acc.flags = read_only ? hipMemAccessFlagsProtRead : hipMemAccessFlagsProtReadWrite;
     hipError_t e = hipMemSetAccess((void *)(uintptr_t)va, bytes, &acc, 1);
-    return e == hipSuccess ? GMS_OK : fail_hip(e, "hipMemSetAccess");
+    if (e == hipSuccess) return GMS_OK;
+    return fail(GMS_ERR_HIP, "hipMemSetAccess(va %#llx, %llu bytes, %s; reservation %#llx + %llu, granularity %llu): %s (%d)",
+                (unsigned long long)va, (unsigned long long)bytes, read_only ? "read-only" : "read-write",
+                (unsigned long long)p->base, (unsigned long long)p->reserved, (unsigned long long)p->gran,
+                hipGetErrorString(e), (int)e);
 }
 
 // Creates physical memory for mapping `m` at `va` and maps it read-write.
@@ -83,7 +87,8 @@ int back(gms_pool *p, uint64_t va, Mapping &m)
     }
     if ((e = hipMemMap((void *)(uintptr_t)va, m.bytes, 0, m.handle, 0)) != hipSuccess) {
         (void)hipMemRelease(m.handle);
-        return fail_hip(e, "hipMemMap");
+        return fail(GMS_ERR_HIP, "hipMemMap(va %#llx, %llu bytes; reservation %#llx): %s (%d)", (unsigned long long)va,
+                    (unsigned long long)m.bytes, (unsigned long long)p->base, hipGetErrorString(e), (int)e);
     }
     int rc = set_access(p, va, m.bytes, false);
     if (rc != GMS_OK) {

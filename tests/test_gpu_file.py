@@ -56,6 +56,37 @@ def test_file_round_trip(tmp_path, flags, staging):
     assert np.array_equal(to_u64(blk2, m.num_blocks), o_blk) and np.array_equal(to_u64(ten2, m.num_entries), o_ten)
 
 
+@pytest.mark.parametrize("io_threads", [1, 7, 64])
+def test_file_pieces_and_short_slices(tmp_path, io_threads):
+    """Slices of several 16 MiB pieces plus a short one, a single device slot
+    (two host slots), and worker counts from one to more than there are pieces."""
+    need_gpu()
+    sizes = [33 << 20, 5, (21 << 20) + 12345, 0, 4096 * 7 + 3, 36 << 20]
+    arena = Arena(sizes, misalign=[0, 1, 0, 0, 8, 0], seed=11)
+    datas = random_datas(sizes, seed=61)
+    arena.fill(datas)
+    m = gms.Manifest(arena.entries, device=0)
+    m.set_staging(40 << 20, 1)  # pieces 16 + 16 + 8 MiB per slice; last slice shorter
+    path = tmp_path / "pieces.bin"
+    blk = u64_dev(m.num_blocks)
+    gms.snapshot_to_file(m, path, flags=gms.FILE_DIRECT, io_threads=io_threads, blk_hash=blk)
+    torch.cuda.synchronize()
+    o_img = oracle.pack(datas)
+    o_blk, o_ten = oracle.hashes(datas)
+    assert m.image_bytes > 2 * (40 << 20) and m.image_bytes % (40 << 20) != 0
+    assert np.array_equal(np.fromfile(path, dtype=np.uint8), o_img), "file != oracle image"
+    assert np.array_equal(to_u64(blk, m.num_blocks), o_blk)
+    for flags in (gms.FILE_DIRECT, 0):
+        arena.poison()
+        ten, cnt = u64_dev(m.num_entries), u64_dev(1)
+        gms.restore_from_file(m, path, flags=flags, io_threads=io_threads, expected=from_u64(o_blk), ten_hash=ten,
+                              mismatch_count=cnt)
+        torch.cuda.synchronize()
+        back, whole = arena.read()
+        assert all(np.array_equal(a, b) for a, b in zip(back, datas)) and arena.outside_untouched(whole)
+        assert to_u64(cnt)[0] == 0 and np.array_equal(to_u64(ten, m.num_entries), o_ten)
+
+
 @pytest.mark.parametrize("offset", [8192, 100])
 def test_file_offset_and_corruption(tmp_path, offset):
     need_gpu()
