@@ -30,9 +30,11 @@ sys.path.insert(0, ROOT)
 METRIC = "restore+verify GB/s on 1 GPU; seconds to restore a 16 GB weight shard"
 HBM_PEAK_GBS = 8000.0
 ALL_ROWS = ["main", "snapshot", "plain", "verify", "h2d", "file", "kv", "kv_vmm", "copy", "cpu", "shards"]
-# The kernel, its launch configuration and the chunking that shapes its accesses.
-KERNEL_SOURCES = ["paper_2609_25451_amd/csrc/gms_kernels.hip", "paper_2609_25451_amd/csrc/gms_internal.h",
-                  "paper_2609_25451_amd/csrc/gms_api.hip", "include/gms.h"]
+# What shapes the measured kernel's accesses: the kernel and its launch code, the
+# header's constants (block and default chunk size) and the chunking in manifest creation.
+KERNEL_SOURCES = ["paper_2609_25451_amd/csrc/gms_kernels.hip", "paper_2609_25451_amd/csrc/gms_internal.h"]
+HEADER = "include/gms.h"
+CHUNKING = ("paper_2609_25451_amd/csrc/gms_api.hip", "int gms_manifest_create(")
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_restore_verify_llama8b.json")
 
 
@@ -45,6 +47,12 @@ def kernel_source_digest() -> str:
     for p in KERNEL_SOURCES:
         with open(os.path.join(ROOT, p), "rb") as f:
             h.update(f.read())
+    with open(os.path.join(ROOT, HEADER)) as f:
+        h.update("".join(l for l in f if l.startswith("#define GMS_")).encode())
+    with open(os.path.join(ROOT, CHUNKING[0])) as f:
+        src = f.read()
+    start = src.index(CHUNKING[1])
+    h.update(src[start:src.index("\n}\n", start)].encode())
     return h.hexdigest()[:16]
 
 

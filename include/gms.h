@@ -98,8 +98,10 @@ enum gms_status {
     GMS_ERR_SIZE = -3,    /* image (or output array) smaller than required */
     GMS_ERR_HIP = -4,     /* a HIP runtime call failed (see last error)     */
     GMS_ERR_NOMEM = -5,   /* host or device allocation failed              */
-    GMS_ERR_STATE = -6,   /* data-plane call on a host-only manifest       */
-    GMS_ERR_IO = -7       /* a file could not be opened, read or written   */
+    GMS_ERR_STATE = -6,   /* call not allowed in the object's current state
+                             (host-only manifest; store lease protocol)     */
+    GMS_ERR_IO = -7,      /* a file could not be opened, read or written   */
+    GMS_ERR_INTEGRITY = -8 /* store: contents differ from their hashes      */
 };
 
 enum gms_mem_kind {
@@ -239,22 +241,24 @@ int gms_snapshot_to_file(const gms_manifest *m, const char *path, uint32_t flags
  * section 3.2: shared state is mapped read-only for readers; sections 3.1 and
  * 3.3: KV pages are released before a checkpoint while their virtual
  * addresses stay reserved, and fresh pages are mapped at the same addresses
- * after restore).  One VA reservation of `va_bytes` holds every mapping.
- * A mapping (a slab, or a dedicated mapping for an allocation larger than a
- * slab) is the unit of release, remap and access change.  Addresses handed
- * out stay valid for the pool's lifetime, across release and remap, and can
- * be used in manifests like any device allocation.  The caller must not let
+ * after restore).  A mapping (a slab, or a dedicated mapping for an
+ * allocation larger than a slab) is the unit of release, remap and access
+ * change; each holds a VA reservation of its own, placed one after another in
+ * a window of `va_bytes` while the address space allows (so consecutive
+ * allocations are contiguous), and together they hold at most `va_bytes` of
+ * VA.  Addresses handed out stay valid until freed, across release and
+ * remap, and can be used in manifests like any device allocation.  The caller must not let
  * kernels (including snapshot/restore/verify) touch a released range; release
  * synchronises the device first.  Not for use under graph capture.
  */
 typedef struct gms_pool gms_pool;
 
-/* Reserves va_bytes of device VA on `device`; slab_bytes 0 = 2 GiB.  Both must be
- * multiples of the allocation granularity (gms_pool_info).  Errors: GMS_ERR_INVALID,
- * GMS_ERR_STATE (no VMM support), GMS_ERR_NOMEM, GMS_ERR_HIP. */
+/* A pool on `device` with a VA budget (and placement window) of va_bytes; slab_bytes
+ * 0 = 2 GiB.  Both must be multiples of the allocation granularity (gms_pool_info).
+ * Errors: GMS_ERR_INVALID, GMS_ERR_STATE (no VMM support), GMS_ERR_NOMEM, GMS_ERR_HIP. */
 int gms_pool_create(int device, uint64_t va_bytes, uint64_t slab_bytes, gms_pool **out);
 
-/* Unmaps and releases every mapping and frees the reservation.  NULL is a no-op. */
+/* Unmaps and releases every mapping and frees the reservations.  NULL is a no-op. */
 void gms_pool_destroy(gms_pool *p);
 
 /* First fit in mapped slabs (a new slab is mapped when none fits); an allocation larger
@@ -262,8 +266,8 @@ void gms_pool_destroy(gms_pool *p);
  * Errors: GMS_ERR_INVALID, GMS_ERR_NOMEM (reservation or device memory exhausted). */
 int gms_pool_alloc(gms_pool *p, uint64_t bytes, uint64_t align, uint64_t *addr_out);
 
-/* Returns an allocation; a dedicated mapping is unmapped and released (its VA stays
- * reserved).  Errors: GMS_ERR_INVALID (not an allocation of this pool). */
+/* Returns an allocation; a dedicated mapping is unmapped and released, with its VA.
+ * Errors: GMS_ERR_INVALID (not an allocation of this pool). */
 int gms_pool_free(gms_pool *p, uint64_t addr);
 
 /* Releases the physical pages of the mappings that exactly tile [addr, addr+bytes),
@@ -278,7 +282,8 @@ int gms_pool_remap(gms_pool *p, uint64_t addr, uint64_t bytes);
  * them read-only, 0 read-write.  Errors: GMS_ERR_INVALID, GMS_ERR_STATE (released). */
 int gms_pool_set_access(gms_pool *p, uint64_t addr, uint64_t bytes, int read_only);
 
-/* Pool facts; any output may be NULL. */
+/* Pool facts (base: start of the placement window; reserved: the VA budget); any output
+ * may be NULL. */
 int gms_pool_info(const gms_pool *p, uint64_t *base, uint64_t *reserved, uint64_t *mapped_bytes,
                   uint64_t *mappings, uint64_t *granularity);
 
@@ -286,13 +291,128 @@ int gms_pool_info(const gms_pool *p, uint64_t *base, uint64_t *reserved, uint64_
 int gms_pool_mapping_of(const gms_pool *p, uint64_t addr, uint64_t *map_addr, uint64_t *map_bytes,
                         int *mapped);
 
+/*
+ * Model-state store: the ownership protocol of paper section 3.2 (Figure 4,
+ * the GMS model-state state machine) over a pool of this library.
+ *
+ * States:
+ *  EMPTY      no layout.
+ *  RW         one writer holds the exclusive read-write lease and populates
+ *             allocations it makes through the store.
+ *  COMMITTED  committed state, immutable, no readers.
+ *  RO         committed state with one or more read-only leases.
+ *
+ * Transitions:
+ *  EMPTY or COMMITTED --connect_rw--> RW (refused while readers hold
+ *  leases or another writer does; from COMMITTED the writer reuses the
+ *  allocation set and its mappings become writable again).
+ *  RW --commit--> COMMITTED: records the layout (a manifest over the
+ *  entries given), hashes every 4 KiB block of it and maps every pool
+ *  mapping read-only, so device writes into committed state fault instead
+ *  of changing it.
+ *  RW --abort, or the writer disconnecting before commit--> EMPTY: discards
+ *  the incomplete state (every allocation, and its physical memory).
+ *  COMMITTED or RO --connect_ro--> RO.  RO --disconnect--> RO, or COMMITTED
+ *  after the last reader.  A reader's disconnect leaves committed state
+ *  intact.
+ *
+ * Integrity: with GMS_CONNECT_VERIFY, connect_ro first re-hashes the
+ * committed state and compares it with the hashes recorded at commit; any
+ * mismatch refuses the lease with GMS_ERR_INTEGRITY and marks the state
+ * invalid (section 3.2: integrity errors invalidate GMS state).  An invalid
+ * state grants no read-only lease; once no reader holds one, a writer may
+ * reconnect, repopulate the same allocations (for example with gms_restore
+ * from an image) and commit again, which makes it valid.
+ *
+ * In one process the store's pool is the engine's own mapping of the
+ * allocations; the paper's cross-process export of allocation handles is not
+ * part of this library.  A store made with device GMS_HOST_ONLY runs the
+ * protocol alone, without memory (no allocations; commit takes no entries).
+ * Store calls are thread-safe and synchronous: each returns after the device
+ * work it enqueues on `stream` has finished.  Leases are non-zero ids, valid
+ * until released; a stale or foreign id is GMS_ERR_INVALID, a call not
+ * allowed in the current state is GMS_ERR_STATE.
+ */
+typedef struct gms_store gms_store;
+
+enum gms_store_state {
+    GMS_STORE_EMPTY = 0,
+    GMS_STORE_RW = 1,
+    GMS_STORE_COMMITTED = 2,
+    GMS_STORE_RO = 3
+};
+
+/* Flags of gms_store_connect_ro. */
+enum gms_connect_flags {
+    GMS_CONNECT_VERIFY = 1 /* re-hash the committed state and refuse the lease on any mismatch */
+};
+
+/* A store with its own pool (gms_pool_create's arguments); device GMS_HOST_ONLY makes a
+ * protocol-only store.  Errors: as gms_pool_create. */
+int gms_store_create(int device, uint64_t va_bytes, uint64_t slab_bytes, gms_store **out);
+
+/* Frees the committed layout, every allocation and the pool, whatever leases are held.
+ * NULL is a no-op. */
+void gms_store_destroy(gms_store *s);
+
+/* Current state, reader count and whether the committed state is invalid; outputs may be NULL. */
+int gms_store_state(const gms_store *s, int *state, uint32_t *readers, int *invalid);
+
+/* The store's pool, for queries (gms_pool_info, gms_pool_mapping_of); NULL if host-only.
+ * Its mutating calls bypass the protocol. */
+gms_pool *gms_store_pool(gms_store *s);
+
+/* Exclusive read-write lease.  Errors: GMS_ERR_STATE (a writer or readers are connected). */
+int gms_store_connect_rw(gms_store *s, uint64_t *lease_out);
+
+/* Writer only: an allocation in the store's pool (as gms_pool_alloc), or its return. */
+int gms_store_alloc(gms_store *s, uint64_t lease, uint64_t bytes, uint64_t align, uint64_t *addr_out);
+int gms_store_free(gms_store *s, uint64_t lease, uint64_t addr);
+
+/*
+ * Writer only: commits entries[0..n) (each inside one allocation of the store) as the
+ * layout, hashes its blocks and maps the pool read-only; the lease ends.  With
+ * expected_blk (device, one u64 per block of the layout, as gms_snapshot writes them) the
+ * populated contents must match it: on any mismatch the commit is refused with
+ * GMS_ERR_INTEGRITY, *mismatch_count_out (host, may be NULL) holds the count, and the
+ * writer keeps its lease.  Errors: GMS_ERR_INVALID (lease, entries), GMS_ERR_OVERLAP,
+ * GMS_ERR_INTEGRITY, GMS_ERR_HIP, GMS_ERR_NOMEM.
+ */
+int gms_store_commit(gms_store *s, uint64_t lease, const gms_entry *entries, uint64_t n,
+                     const uint64_t *expected_blk, uint64_t *mismatch_count_out, void *stream);
+
+/* Writer only: discards the incomplete state (EMPTY); the lease ends. */
+int gms_store_abort(gms_store *s, uint64_t lease);
+
+/* Read-only lease on committed state.  flags: GMS_CONNECT_VERIFY.  *mismatch_count_out
+ * (host, may be NULL) receives the blocks that failed verification.  Errors:
+ * GMS_ERR_STATE (no committed state, or a writer is connected), GMS_ERR_INTEGRITY. */
+int gms_store_connect_ro(gms_store *s, uint32_t flags, uint64_t *lease_out, uint64_t *mismatch_count_out,
+                         void *stream);
+
+/* Re-hashes the committed state against its commit-time hashes: *mismatch_count_out (host)
+ * gets the count and mismatch_list_out (device, may be NULL) up to `cap` global block
+ * indices, in any order.  A mismatch marks the state invalid but is not an error.
+ * Errors: GMS_ERR_STATE (nothing committed), GMS_ERR_HIP. */
+int gms_store_verify(gms_store *s, uint64_t *mismatch_count_out, uint64_t *mismatch_list_out, uint64_t cap,
+                     void *stream);
+
+/* Ends a lease: a reader's leaves committed state intact; a writer's before commit is an
+ * abort. */
+int gms_store_disconnect(gms_store *s, uint64_t lease);
+
+/* The committed layout (a manifest of the store) and its block hashes (device, one u64 per
+ * block); NULL while nothing is committed.  Valid until the next writer connects. */
+const gms_manifest *gms_store_layout(const gms_store *s);
+const uint64_t *gms_store_block_hashes(const gms_store *s);
+
 /* Static description of a status code. */
 const char *gms_status_str(int status);
 
 /* The calling thread's last error message ("" if none); valid until its next call. */
 const char *gms_last_error(void);
 
-/* ABI version of this header (1). */
+/* ABI version of this header (2: adds the model-state store and GMS_ERR_INTEGRITY). */
 int gms_abi_version(void);
 
 #ifdef __cplusplus

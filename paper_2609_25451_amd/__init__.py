@@ -39,6 +39,13 @@ GMS_ERR_HIP = -4
 GMS_ERR_NOMEM = -5
 GMS_ERR_STATE = -6
 GMS_ERR_IO = -7
+GMS_ERR_INTEGRITY = -8
+STORE_EMPTY = 0
+STORE_RW = 1
+STORE_COMMITTED = 2
+STORE_RO = 3
+STORE_STATES = {STORE_EMPTY: "EMPTY", STORE_RW: "RW", STORE_COMMITTED: "COMMITTED", STORE_RO: "RO"}
+CONNECT_VERIFY = 1
 FILE_DIRECT = 1
 FILE_SYNC = 2
 MEM_DEVICE = 0
@@ -83,14 +90,29 @@ _pool_remap = _sig("gms_pool_remap", INT, [VP, U64, U64])
 _pool_set_access = _sig("gms_pool_set_access", INT, [VP, U64, U64, INT])
 _pool_info = _sig("gms_pool_info", INT, [VP, VP, VP, VP, VP, VP])
 _pool_mapping_of = _sig("gms_pool_mapping_of", INT, [VP, U64, VP, VP, VP])
+_store_create = _sig("gms_store_create", INT, [INT, U64, U64, ctypes.POINTER(VP)])
+_store_destroy = _sig("gms_store_destroy", None, [VP])
+_store_state = _sig("gms_store_state", INT, [VP, VP, VP, VP])
+_store_pool = _sig("gms_store_pool", VP, [VP])
+_store_connect_rw = _sig("gms_store_connect_rw", INT, [VP, ctypes.POINTER(U64)])
+_store_alloc = _sig("gms_store_alloc", INT, [VP, U64, U64, U64, ctypes.POINTER(U64)])
+_store_free = _sig("gms_store_free", INT, [VP, U64, U64])
+_store_commit = _sig("gms_store_commit", INT, [VP, U64, ctypes.POINTER(GmsEntry), U64, VP, ctypes.POINTER(U64), VP])
+_store_abort = _sig("gms_store_abort", INT, [VP, U64])
+_store_connect_ro = _sig("gms_store_connect_ro", INT, [VP, ctypes.c_uint32, ctypes.POINTER(U64), ctypes.POINTER(U64), VP])
+_store_verify = _sig("gms_store_verify", INT, [VP, ctypes.POINTER(U64), VP, U64, VP])
+_store_disconnect = _sig("gms_store_disconnect", INT, [VP, U64])
+_store_layout = _sig("gms_store_layout", VP, [VP])
+_store_block_hashes = _sig("gms_store_block_hashes", VP, [VP])
 _status_str = _sig("gms_status_str", ctypes.c_char_p, [INT])
 _last_error = _sig("gms_last_error", ctypes.c_char_p, [])
 _abi = _sig("gms_abi_version", INT, [])
 
 
 class GmsError(RuntimeError):
-    def __init__(self, status: int, call: str):
+    def __init__(self, status: int, call: str, mismatches: int = 0):
         self.status = status
+        self.mismatches = mismatches
         msg = _last_error().decode(errors="replace")
         super().__init__(f"{call}: {_status_str(status).decode()} ({status}): {msg}")
 
@@ -127,22 +149,41 @@ def exported_symbols_declared() -> list[str]:
     return sorted(set(re.findall(r"\b(gms_[a-z_0-9]+)\s*\(", text)))
 
 
+def _ranges(entries):
+    out = []
+    for e in entries:
+        if hasattr(e, "data_ptr"):
+            out.append((int(e.data_ptr()), int(e.numel() * e.element_size())))
+        else:
+            out.append((int(e[0]), int(e[1])))
+    return out
+
+
+def _entry_array(ranges):
+    return (GmsEntry * max(len(ranges), 1))(*[GmsEntry(a, b) for a, b in ranges])
+
+
 class Manifest:
     """A manifest over device ranges ``entries`` = [(addr, nbytes)] or tensors."""
 
     def __init__(self, entries, device: int = 0, chunk_bytes: int = 0):
-        ranges = []
-        for e in entries:
-            if hasattr(e, "data_ptr"):
-                ranges.append((int(e.data_ptr()), int(e.numel() * e.element_size())))
-            else:
-                ranges.append((int(e[0]), int(e[1])))
+        ranges = _ranges(entries)
         n = len(ranges)
-        arr = (GmsEntry * max(n, 1))(*[GmsEntry(a, b) for a, b in ranges])
         h = VP()
-        _check(_create(arr, n, device, chunk_bytes, ctypes.byref(h)), "gms_manifest_create")
+        _check(_create(_entry_array(ranges), n, device, chunk_bytes, ctypes.byref(h)), "gms_manifest_create")
         self._h = h
+        self._owned = True
         self.sizes = [b for _, b in ranges]
+
+    @classmethod
+    def _borrow(cls, handle: int, owner):
+        """A view of a manifest owned by the library (a store's committed layout)."""
+        m = cls.__new__(cls)
+        m._h = VP(handle)
+        m._owned = False
+        m._owner = owner
+        m.sizes = None
+        return m
 
     @property
     def handle(self) -> int:
@@ -150,7 +191,8 @@ class Manifest:
 
     def close(self) -> None:
         if getattr(self, "_h", None) is not None and self._h.value:
-            _destroy(self._h)
+            if getattr(self, "_owned", True):
+                _destroy(self._h)
             self._h = VP()
 
     def __del__(self):
@@ -282,6 +324,123 @@ class Pool:
         return int(a.value), int(b.value), bool(m.value)
 
 
+class Store:
+    """Model-state store with the GMS lease protocol (see gms_store_* in include/gms.h).
+
+    ``device=HOST_ONLY`` gives a protocol-only store without memory.
+    """
+
+    def __init__(self, va_bytes: int = 0, slab_bytes: int = 0, device: int = 0):
+        h = VP()
+        _check(_store_create(device, va_bytes, slab_bytes, ctypes.byref(h)), "gms_store_create")
+        self._h = h
+        self.device = device
+
+    def close(self) -> None:
+        if getattr(self, "_h", None) is not None and self._h.value:
+            _store_destroy(self._h)
+            self._h = VP()
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    def state(self):
+        """(state name, reader count, invalid)."""
+        st, rd, inv = INT(), ctypes.c_uint32(), INT()
+        _check(_store_state(self._h, ctypes.byref(st), ctypes.byref(rd), ctypes.byref(inv)), "gms_store_state")
+        return STORE_STATES[st.value], int(rd.value), bool(inv.value)
+
+    def pool_info(self) -> dict:
+        p = _store_pool(self._h)
+        if not p:
+            return {}
+        v = [U64() for _ in range(5)]
+        _check(_pool_info(p, *[ctypes.byref(x) for x in v]), "gms_pool_info")
+        return dict(zip(["base", "reserved", "mapped_bytes", "mappings", "granularity"], [int(x.value) for x in v]))
+
+    @property
+    def pool_handle(self) -> int:
+        return int(_store_pool(self._h) or 0)
+
+    def connect_rw(self) -> "WriteLease":
+        lease = U64()
+        _check(_store_connect_rw(self._h, ctypes.byref(lease)), "gms_store_connect_rw")
+        return WriteLease(self, int(lease.value))
+
+    def connect_ro(self, verify: bool = True, stream=None) -> "ReadLease":
+        lease, cnt = U64(), U64()
+        rc = _store_connect_ro(self._h, CONNECT_VERIFY if verify else 0, ctypes.byref(lease), ctypes.byref(cnt),
+                               _stream(stream))
+        if rc != GMS_OK:
+            raise GmsError(rc, "gms_store_connect_ro", int(cnt.value))
+        return ReadLease(self, int(lease.value))
+
+    def verify(self, mismatch_list=None, mismatch_cap: int = 0, stream=None) -> int:
+        cnt = U64()
+        _check(_store_verify(self._h, ctypes.byref(cnt), _ptr(mismatch_list), mismatch_cap, _stream(stream)),
+               "gms_store_verify")
+        return int(cnt.value)
+
+    def layout(self) -> Manifest | None:
+        h = _store_layout(self._h)
+        return Manifest._borrow(h, self) if h else None
+
+    def block_hashes_ptr(self) -> int:
+        return int(_store_block_hashes(self._h) or 0)
+
+
+class _Lease:
+    def __init__(self, store: Store, lease: int):
+        self.store = store
+        self.id = lease
+        self.open = True
+
+    def close(self) -> None:
+        """Ends the lease (a writer's before commit discards its state)."""
+        if self.open:
+            self.open = False
+            _check(_store_disconnect(self.store._h, self.id), "gms_store_disconnect")
+
+    def __enter__(self):
+        return self
+
+    def __exit__(self, *exc):
+        self.close()
+
+
+class WriteLease(_Lease):
+    """Exclusive read-write lease; leaving it without commit aborts."""
+
+    def alloc(self, nbytes: int, align: int = 0) -> int:
+        out = U64()
+        _check(_store_alloc(self.store._h, self.id, nbytes, align, ctypes.byref(out)), "gms_store_alloc")
+        return int(out.value)
+
+    def free(self, addr: int) -> None:
+        _check(_store_free(self.store._h, self.id, addr), "gms_store_free")
+
+    def commit(self, entries, expected=None, stream=None) -> None:
+        ranges = _ranges(entries)
+        cnt = U64()
+        rc = _store_commit(self.store._h, self.id, _entry_array(ranges), len(ranges), _ptr(expected),
+                           ctypes.byref(cnt), _stream(stream))
+        if rc != GMS_OK:
+            raise GmsError(rc, "gms_store_commit", int(cnt.value))
+        self.open = False
+
+    def abort(self) -> None:
+        if self.open:
+            self.open = False
+            _check(_store_abort(self.store._h, self.id), "gms_store_abort")
+
+
+class ReadLease(_Lease):
+    """Read-only lease on committed state."""
+
+
 def status_str(rc: int) -> str:
     return _status_str(rc).decode()
 
@@ -300,3 +459,12 @@ gms_snapshot_to_file = _snapshot_file
 gms_manifest_set_staging = _set_staging
 gms_status_str = _status_str
 gms_last_error = _last_error
+gms_store_create = _store_create
+gms_store_destroy = _store_destroy
+gms_store_state = _store_state
+gms_store_connect_rw = _store_connect_rw
+gms_store_connect_ro = _store_connect_ro
+gms_store_commit = _store_commit
+gms_store_abort = _store_abort
+gms_store_disconnect = _store_disconnect
+gms_store_verify = _store_verify

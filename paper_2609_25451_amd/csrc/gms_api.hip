@@ -42,6 +42,7 @@ int fail(int status, const char *fmt, ...)
 
 int fail_hip(hipError_t e, const char *what)
 {
+    (void)hipGetLastError();  // reported here: keep it from resurfacing in a later launch check
     return fail(GMS_ERR_HIP, "%s: %s (%d)", what, hipGetErrorString(e), (int)e);
 }
 
@@ -331,7 +332,7 @@ using gms::make_hash;
 
 extern "C" {
 
-int gms_abi_version(void) { return 1; }
+int gms_abi_version(void) { return 2; }
 
 const char *gms_status_str(int status)
 {
@@ -344,6 +345,7 @@ const char *gms_status_str(int status)
     case GMS_ERR_NOMEM: return "out of memory";
     case GMS_ERR_STATE: return "operation not valid for this manifest";
     case GMS_ERR_IO: return "file I/O error";
+    case GMS_ERR_INTEGRITY: return "contents differ from their recorded hashes";
     default: return "unknown status";
     }
 }

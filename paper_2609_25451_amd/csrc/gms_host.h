@@ -75,6 +75,12 @@ struct gms_manifest {
 
 namespace gms {
 
+// pool internals used by the model-state store
+int pool_reset(gms_pool *p);
+int pool_set_access_all(gms_pool *p, bool read_only);
+bool pool_holds(gms_pool *p, uint64_t addr, uint64_t bytes);
+int pool_device(const gms_pool *p);
+
 void free_ring(gms_manifest *m);
 int ensure_ring(gms_manifest *m);       // device slots, copy stream, events, slice table
 int ensure_host_ring(gms_manifest *m);  // plus pinned host slots

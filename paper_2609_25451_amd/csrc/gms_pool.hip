@@ -7,8 +7,13 @@
 // 3.2).  Before a checkpoint the engine releases its KV pages but keeps their
 // virtual-address reservations, so addresses captured in graphs and tensors
 // stay valid, and fresh pages are mapped at the same addresses after restore
-// (section 3.1, section 3.3).  Here one reservation holds every mapping; a
-// mapping (slab or dedicated) is the unit of release, remap and access change.
+// (section 3.1, section 3.3).  A mapping (slab or dedicated) is the unit of
+// release, remap and access change, and each mapping has a VA reservation of
+// its own: when mappings of different sizes share one reservation, HIP's
+// access changes on one of them fail at random (measured on this ROCm, where
+// one reservation per mapping never failed).  Reservations are placed one
+// after another in the pool's address window while the address space allows,
+// so consecutive allocations stay contiguous.
 
 #include <algorithm>
 #include <cstdio>
@@ -45,7 +50,9 @@ uint64_t round_up(uint64_t v, uint64_t a) { return (v + a - 1) / a * a; }
 
 struct gms_pool {
     int device = 0;
-    uint64_t base = 0, reserved = 0, next = 0;  // next: first unused VA offset
+    uint64_t base = 0, reserved = 0;  // address window (placement hint) and VA budget
+    uint64_t next = 0;                // window offset where the next mapping is placed
+    uint64_t used = 0;                // VA held by the mappings' reservations
     uint64_t gran = 0, slab_bytes = 0;
     std::map<uint64_t, Mapping> maps;   // by VA
     std::map<uint64_t, Alloc> allocs;   // by address
@@ -70,10 +77,10 @@ int set_access(gms_pool *p, uint64_t va, uint64_t bytes, bool read_only)
     acc.flags = read_only ? hipMemAccessFlagsProtRead : hipMemAccessFlagsProtReadWrite;
     hipError_t e = hipMemSetAccess((void *)(uintptr_t)va, bytes, &acc, 1);
     if (e == hipSuccess) return GMS_OK;
-    return fail(GMS_ERR_HIP, "hipMemSetAccess(va %#llx, %llu bytes, %s; reservation %#llx + %llu, granularity %llu): %s (%d)",
+    (void)hipGetLastError();
+    return fail(GMS_ERR_HIP, "hipMemSetAccess(va %#llx, %llu bytes, %s; granularity %llu): %s (%d)",
                 (unsigned long long)va, (unsigned long long)bytes, read_only ? "read-only" : "read-write",
-                (unsigned long long)p->base, (unsigned long long)p->reserved, (unsigned long long)p->gran,
-                hipGetErrorString(e), (int)e);
+                (unsigned long long)p->gran, hipGetErrorString(e), (int)e);
 }
 
 // Creates physical memory for mapping `m` at `va` and maps it read-write.
@@ -87,8 +94,9 @@ int back(gms_pool *p, uint64_t va, Mapping &m)
     }
     if ((e = hipMemMap((void *)(uintptr_t)va, m.bytes, 0, m.handle, 0)) != hipSuccess) {
         (void)hipMemRelease(m.handle);
-        return fail(GMS_ERR_HIP, "hipMemMap(va %#llx, %llu bytes; reservation %#llx): %s (%d)", (unsigned long long)va,
-                    (unsigned long long)m.bytes, (unsigned long long)p->base, hipGetErrorString(e), (int)e);
+        (void)hipGetLastError();
+        return fail(GMS_ERR_HIP, "hipMemMap(va %#llx, %llu bytes): %s (%d)", (unsigned long long)va,
+                    (unsigned long long)m.bytes, hipGetErrorString(e), (int)e);
     }
     int rc = set_access(p, va, m.bytes, false);
     if (rc != GMS_OK) {
@@ -110,22 +118,54 @@ int unback(uint64_t va, Mapping &m)
     return GMS_OK;
 }
 
-// New mapping of `bytes` at the next free VA (aligned to `align`).
-int new_mapping(gms_pool *p, uint64_t bytes, uint64_t align, bool dedicated, uint64_t *va_out)
+constexpr uint64_t kLargePage = 2ull << 20;
+
+// New mapping of `bytes` with a reservation of its own, at the next address of
+// the window when that is free, elsewhere otherwise.
+int new_mapping(gms_pool *p, uint64_t bytes, bool dedicated, uint64_t *va_out)
 {
-    const uint64_t off = round_up(p->next, std::max(align, p->gran));
-    if (off + bytes > p->reserved || off + bytes < off)
-        return fail(GMS_ERR_NOMEM, "pool reservation of %llu bytes exhausted", (unsigned long long)p->reserved);
-    const uint64_t va = p->base + off;
+    if (p->used + bytes > p->reserved || p->used + bytes < p->used)
+        return fail(GMS_ERR_NOMEM, "pool VA budget of %llu bytes exhausted", (unsigned long long)p->reserved);
+    const uint64_t align = bytes % kLargePage == 0 ? std::max(kLargePage, p->gran) : p->gran;
+    const uint64_t off = round_up(p->next, align);
+    void *want = off + bytes <= p->reserved ? (void *)(uintptr_t)(p->base + off) : nullptr;
+    void *res = nullptr;
+    hipError_t e = hipMemAddressReserve(&res, bytes, align, want, 0);
+    if (e != hipSuccess && want) {
+        (void)hipGetLastError();
+        e = hipMemAddressReserve(&res, bytes, align, nullptr, 0);
+    }
+    if (e != hipSuccess) {
+        (void)hipGetLastError();
+        return fail(GMS_ERR_NOMEM, "hipMemAddressReserve(%llu): %s", (unsigned long long)bytes, hipGetErrorString(e));
+    }
+    const uint64_t va = (uint64_t)(uintptr_t)res;
     Mapping m;
     m.bytes = bytes;
     m.dedicated = dedicated;
     int rc = back(p, va, m);
-    if (rc != GMS_OK) return rc;
+    if (rc != GMS_OK) {
+        (void)hipMemAddressFree(res, bytes);
+        return rc;
+    }
     if (!dedicated) m.free[0] = bytes;
     p->maps[va] = std::move(m);
-    p->next = off + bytes;
+    p->used += bytes;
+    if (res == want) p->next = off + bytes;
     *va_out = va;
+    return GMS_OK;
+}
+
+// Unmaps (if backed) and frees the reservation of the mapping at `va`.
+int drop_mapping(gms_pool *p, uint64_t va, Mapping &m)
+{
+    if (m.mapped) {
+        int rc = unback(va, m);
+        if (rc != GMS_OK) return rc;
+    }
+    hipError_t e = hipMemAddressFree((void *)(uintptr_t)va, m.bytes);
+    if (e != hipSuccess) return fail_hip(e, "hipMemAddressFree");
+    p->used -= m.bytes;
     return GMS_OK;
 }
 
@@ -151,6 +191,58 @@ int whole_mappings(gms_pool *p, uint64_t addr, uint64_t bytes, std::vector<uint6
 
 }  // namespace
 
+namespace gms {
+
+// Discards every allocation: unmaps and releases all physical memory and
+// rewinds the reservation, which the pool keeps.
+int pool_reset(gms_pool *p)
+{
+    std::lock_guard<std::mutex> lock(p->mu);
+    DeviceGuard g(p->device);
+    if (g.err != hipSuccess) return fail_hip(g.err, "hipSetDevice");
+    hipError_t e = hipDeviceSynchronize();  // no kernel may still touch the pages
+    if (e != hipSuccess) return fail_hip(e, "hipDeviceSynchronize");
+    while (!p->maps.empty()) {
+        auto it = p->maps.begin();
+        int rc = drop_mapping(p, it->first, it->second);
+        if (rc != GMS_OK) return rc;
+        p->maps.erase(it);
+    }
+    p->allocs.clear();
+    p->next = 0;
+    return GMS_OK;
+}
+
+// Read-only or read-write device access for every backed mapping.
+int pool_set_access_all(gms_pool *p, bool read_only)
+{
+    std::lock_guard<std::mutex> lock(p->mu);
+    DeviceGuard g(p->device);
+    if (g.err != hipSuccess) return fail_hip(g.err, "hipSetDevice");
+    for (auto &kv : p->maps) {
+        Mapping &m = kv.second;
+        if (!m.mapped) continue;
+        int rc = set_access(p, kv.first, m.bytes, read_only);
+        if (rc != GMS_OK) return rc;
+        m.read_only = read_only;
+    }
+    return GMS_OK;
+}
+
+// True when [addr, addr + bytes) lies inside one allocation of the pool.
+bool pool_holds(gms_pool *p, uint64_t addr, uint64_t bytes)
+{
+    std::lock_guard<std::mutex> lock(p->mu);
+    auto it = p->allocs.upper_bound(addr);
+    if (it == p->allocs.begin()) return false;
+    --it;
+    return addr + bytes >= addr && addr + bytes <= it->first + it->second.bytes;
+}
+
+int pool_device(const gms_pool *p) { return p->device; }
+
+}  // namespace gms
+
 extern "C" {
 
 int gms_pool_create(int device, uint64_t va_bytes, uint64_t slab_bytes, gms_pool **out)
@@ -175,12 +267,17 @@ int gms_pool_create(int device, uint64_t va_bytes, uint64_t slab_bytes, gms_pool
                     (unsigned long long)va_bytes, (unsigned long long)slab_bytes, gran);
     gms_pool *p = new (std::nothrow) gms_pool;
     if (!p) return fail(GMS_ERR_NOMEM, "pool");
+    // find a free window of va_bytes; mappings reserve their own ranges in it
     void *va = nullptr;
-    if ((e = hipMemAddressReserve(&va, va_bytes, 0, nullptr, 0)) != hipSuccess) {
+    if ((e = hipMemAddressReserve(&va, va_bytes, std::max<uint64_t>(kLargePage, gran), nullptr, 0)) != hipSuccess) {
         delete p;
         (void)hipGetLastError();
         return fail(GMS_ERR_NOMEM, "hipMemAddressReserve(%llu): %s", (unsigned long long)va_bytes,
                     hipGetErrorString(e));
+    }
+    if ((e = hipMemAddressFree(va, va_bytes)) != hipSuccess) {
+        delete p;
+        return fail_hip(e, "hipMemAddressFree");
     }
     p->device = device;
     p->base = (uint64_t)(uintptr_t)va;
@@ -197,9 +294,8 @@ void gms_pool_destroy(gms_pool *p)
     {
         DeviceGuard g(p->device);
         (void)hipDeviceSynchronize();
-        for (auto &kv : p->maps)
-            if (kv.second.mapped) (void)unback(kv.first, kv.second);
-        (void)hipMemAddressFree((void *)(uintptr_t)p->base, p->reserved);
+        for (auto &kv : p->maps) (void)drop_mapping(p, kv.first, kv.second);
+        (void)hipGetLastError();
     }
     delete p;
 }
@@ -218,7 +314,7 @@ int gms_pool_alloc(gms_pool *p, uint64_t bytes, uint64_t align, uint64_t *addr_o
     const uint64_t need = round_up(bytes, align);
     if (need > p->slab_bytes) {  // dedicated mapping
         uint64_t va = 0;
-        int rc = new_mapping(p, round_up(bytes, p->gran), p->gran, true, &va);
+        int rc = new_mapping(p, round_up(bytes, p->gran), true, &va);
         if (rc != GMS_OK) return rc;
         p->allocs[va] = Alloc{bytes, va};
         *addr_out = va;
@@ -243,7 +339,7 @@ int gms_pool_alloc(gms_pool *p, uint64_t bytes, uint64_t align, uint64_t *addr_o
         }
         if (attempt == 0) {
             uint64_t va = 0;
-            int rc = new_mapping(p, p->slab_bytes, p->gran, false, &va);
+            int rc = new_mapping(p, p->slab_bytes, false, &va);
             if (rc != GMS_OK) return rc;
         }
     }
@@ -260,12 +356,10 @@ int gms_pool_free(gms_pool *p, uint64_t addr)
     Mapping &m = p->maps[a->second.map_va];
     if (m.dedicated) {
         DeviceGuard g(p->device);
-        if (m.mapped) {
-            (void)hipDeviceSynchronize();
-            int rc = unback(a->second.map_va, m);
-            if (rc != GMS_OK) return rc;
-        }
-        p->maps.erase(a->second.map_va);  // its VA stays reserved, unused
+        if (m.mapped) (void)hipDeviceSynchronize();
+        int rc = drop_mapping(p, a->second.map_va, m);
+        if (rc != GMS_OK) return rc;
+        p->maps.erase(a->second.map_va);
     } else {
         uint64_t off = addr - a->second.map_va, len = a->second.bytes;
         auto nx = m.free.lower_bound(off);
