@@ -8,10 +8,9 @@
 namespace gms {
 
 constexpr uint32_t kBlockBytes = 4096;  // hash block and image alignment
-constexpr int kThreads = 512;           // 8 wave64s per workgroup
 
-// One workgroup's unit of work: a piece of one entry that never crosses an
-// image offset that is a multiple of the manifest's chunk size.
+// An entry of the work list: a piece of one entry that never crosses an image
+// offset that is a multiple of the manifest's chunk size.
 struct Chunk {
     uint64_t addr;   // device address of the piece's first byte
     uint64_t img;    // image offset of the piece's first byte (multiple of 4096)
@@ -36,9 +35,11 @@ struct HashOut {
 // Zeroes the tensor-hash array and the mismatch counter (either may be null).
 hipError_t launch_prologue(const HashOut &h, uint64_t n_entries, hipStream_t s);
 
-// Runs `op` over chunks[first, first + count).  The image byte at offset x
-// lives at img_base + (x - img_origin).  `hash` selects the hashing variant.
+// Runs `op` over chunks[first, first + count) of a manifest whose chunks are
+// at most `chunk_bytes` long.  The image byte at offset x lives at
+// img_base + (x - img_origin).  `hash` selects the hashing variant.
 hipError_t launch_stream(int op, bool hash, const Chunk *chunks, uint64_t first, uint64_t count,
-                         uint8_t *img_base, uint64_t img_origin, const HashOut &h, hipStream_t s);
+                         uint64_t chunk_bytes, uint8_t *img_base, uint64_t img_origin, const HashOut &h,
+                         hipStream_t s);
 
 }  // namespace gms

@@ -1,25 +1,22 @@
 // Gather / scatter / verify kernels for gfx950.
 //
-// One workgroup (8 wave64s) takes one chunk of the manifest's work list; each
-// wave walks the chunk's 4 KiB blocks with stride 8.  For one block a lane
-// moves four 16-byte segments at byte offsets k*1024 + lane*16 (k = 0..3), so
-// every load and store instruction of the wave covers 1 KiB contiguously.
-// Each wave keeps the loads of its next two blocks in flight while it stores
-// and hashes the current one, and restore/snapshot launches reserve enough
-// LDS to hold residency at one workgroup per CU: on MI355X a copy reaches its
-// best HBM efficiency with about eight deep streams per CU rather than many
-// shallow ones (pure reads run at ~90% of peak, pure writes at ~72%).
-// Hashing happens on the registers that were just moved: each lane mixes its
-// eight 8-byte words, the wave XOR-reduces its 64 partials with DPP row
-// operations plus four lane reads, and lane 0 stores / compares the block
-// hash.  Tensor hashes combine the eight waves' XORs in LDS and take one
-// 64-bit atomic XOR per chunk.
+// The unit of work is two 4 KiB blocks of one chunk of the manifest's work
+// list, taken by one 2-wave workgroup: each wave moves and hashes one block.
+// For a block a lane moves four 16-byte segments at byte offsets
+// k*1024 + lane*16 (k = 0..3), so every load and store instruction of the
+// wave covers 1 KiB contiguously.  Small, short-lived workgroups let the
+// dispatcher keep every CU's few resident waves busy; restore and snapshot
+// launches reserve LDS so that six workgroups (12 waves) are resident per CU,
+// which measured best for the mixed read/write stream across weight sets,
+// shards and KV pools, and the unit order is XCD-aware.  Hashing happens on
+// the registers that were just moved: each lane mixes its eight 8-byte words,
+// the wave XOR-reduces its 64 partials with DPP row operations plus four lane
+// reads, and lane 0 stores / compares the block hash.  Tensor hashes combine
+// the two waves' XORs in LDS and take one 64-bit atomic XOR per unit.
 //
 // Bandwidth path: no MFMA; 16-byte non-temporal loads and stores for the
 // streaming side; byte-granular code only for unaligned entries and the ragged
 // last block of an entry.
-
-#include <mutex>
 
 #include "gms_internal.h"
 
@@ -37,8 +34,8 @@ constexpr uint64_t kMulA = 0xBF58476D1CE4E5B9ull;
 constexpr uint64_t kMulB = 0x94D049BB133111EBull;
 constexpr uint64_t kSegStrideG = 128ull * kG;    // word-index step between a lane's segments
 constexpr uint64_t kBlockStrideG = 512ull * kG;  // word-index step between blocks
-constexpr int kWaves = kThreads / 64;            // waves per workgroup
-constexpr int kDepth = 2;                        // blocks each wave keeps loading ahead
+constexpr int kWaves = 2;                        // waves per workgroup, one block each
+constexpr int kUnitThreads = kWaves * 64;
 constexpr uint32_t kXcds = 8;                    // accelerator complex dies on MI355X
 
 __device__ __forceinline__ uint64_t mix64(uint64_t z)
@@ -171,19 +168,16 @@ __device__ __forceinline__ uint32_t fast_blocks(const Chunk &c)
     return (c.addr & 15) == 0 ? c.len / kBlockBytes : 0;
 }
 
-// One chunk per workgroup (the hardware dispatcher balances chunks across
-// CUs and XCDs).  Phase 1 streams the chunk's full, aligned blocks through a
-// software pipeline: each wave keeps the loads of its next kDepth blocks in
-// flight while it stores and hashes the current one.  A block's expected hash
-// is loaded just before the block's data and folded into the wave reduction,
-// so comparing never waits on a load younger than the block itself (vmcnt
-// retires in order, and on CDNA it counts stores too).  Phase 2 handles the ragged last block and every block of
-// an unaligned entry with byte-granular code.  Restore and snapshot launches
-// reserve enough LDS to hold residency at one 8-wave workgroup per CU: about
-// eight deep streams per CU keep mixed read/write HBM traffic efficient.
+// Unit u is blocks [(u mod 2^shift) * kWaves, +kWaves) of chunk u >> shift
+// (2^shift units cover the manifest's chunk size); wave w of the workgroup
+// takes the unit's block w.  A full, aligned block is loaded with 16-byte
+// non-temporal loads, stored and hashed from the same registers; its expected
+// hash is loaded branch-free (a harmless address when not checking) just
+// before its data and folded into the wave reduction.  The ragged last block
+// of an entry and every block of an unaligned entry take byte-granular code.
 template <int OP, bool HASH>
-__global__ void __launch_bounds__(kThreads)
-k_stream(const Chunk *__restrict__ chunks, uint64_t count, gbyte *__restrict__ img_base,
+__global__ void __launch_bounds__(kUnitThreads)
+k_stream(const Chunk *__restrict__ chunks, uint64_t count, uint32_t unit_shift, gbyte *__restrict__ img_base,
          uint64_t img_origin, HashOut h)
 {
     extern __shared__ uint64_t wave_part[];  // kWaves words used
@@ -192,74 +186,43 @@ k_stream(const Chunk *__restrict__ chunks, uint64_t count, gbyte *__restrict__ i
     const uint64_t lane_g = 2ull * lane * kG;  // j*G offset of the lane's first word in a block
     const bool check = HASH && h.expected != nullptr;
     const uint64_t *const exp_dummy = (const uint64_t *)chunks;  // any readable word
+    const uint64_t units = count << unit_shift;
+    const uint32_t unit_mask = (1u << unit_shift) - 1;
 
     // XCD-aware order: the dispatcher hands workgroup IDs to the 8 XCDs round
     // robin, so within each grid-sized round, XCD x takes the x-th contiguous
-    // eighth of the chunks and every XCD streams its own contiguous region of
+    // eighth of the units and every XCD streams its own contiguous region of
     // the image and of the entries.
     const uint64_t per_xcd = gridDim.x / kXcds;  // the grid is a multiple of kXcds
     const uint64_t slot_in_round = (blockIdx.x % kXcds) * per_xcd + blockIdx.x / kXcds;
-    for (uint64_t round = 0; round < count; round += gridDim.x) {
-        const uint64_t ci = round + slot_in_round;
-        if (ci >= count) break;
-        const Chunk c = chunks[ci];
+    for (uint64_t round = 0; round < units; round += gridDim.x) {
+        const uint64_t u = round + slot_in_round;
+        if (u >= units) break;  // uniform across the workgroup
+        const Chunk c = chunks[u >> unit_shift];
+        const uint32_t b = ((uint32_t)u & unit_mask) * kWaves + wave;  // the wave's block of the chunk
         const uint32_t nblk = (c.len + kBlockBytes - 1) / kBlockBytes;
         const uint32_t nfull = fast_blocks(c);
         const bool aligned = (c.addr & 15) == 0;
-        gbyte *const img = img_base + (c.img - img_origin) + lane * 16;
-        gbyte *const ent = (gbyte *)c.addr + lane * 16;
-        gbyte *const src = OP == kRestore ? img : ent;
-        gbyte *const dst = OP == kRestore ? ent : img;
-        const uint64_t jg_chunk = (c.off >> 3) * kG + lane_g;
-        const uint64_t g0 = c.img >> 12;
+        gbyte *const img = img_base + (c.img - img_origin) + (size_t)b * kBlockBytes + lane * 16;
+        gbyte *const ent = (gbyte *)c.addr + (size_t)b * kBlockBytes + lane * 16;
+        const uint64_t jg0 = (c.off >> 3) * kG + (uint64_t)b * kBlockStrideG + lane_g;
+        const uint64_t gblk = (c.img >> 12) + b;
         uint64_t tacc = 0;
 
-        // ---- phase 1: full aligned blocks wave, wave + kWaves, ...
-        // A ring slot is consumed in place (stored and hashed straight from
-        // its registers) and only then reloaded with the wave's block kDepth
-        // steps ahead.  The expected-hash load is branch-free (a harmless
-        // address when not checking) and precedes its block's loads.  Both
-        // keep the compiler from inserting register copies that would wait
-        // for every outstanding load.
-        if (wave < nfull) {
-            const uint32_t mine = (nfull - wave + kWaves - 1) / kWaves;
-            u32x4 ring[kDepth][4];
-            uint64_t want[kDepth];
+        if (b < nfull) {  // full aligned block
+            uint64_t want = 0;
+            if (HASH) want = *(check ? h.expected + gblk : exp_dummy);
+            u32x4 v[4];
+            load_block(v, OP == kRestore ? img : ent);
+            if (OP != kVerify) store_block(v, OP == kRestore ? ent : img);
+            if (HASH) {
+                uint64_t hl = 0;
 #pragma unroll
-            for (int d = 0; d < kDepth; ++d) {
-                if ((uint32_t)d < mine) {
-                    const uint32_t b = wave + d * kWaves;
-                    if (HASH) want[d] = *(check ? h.expected + g0 + b : exp_dummy);
-                    load_block(ring[d], src + (size_t)b * kBlockBytes);
-                }
+                for (int k = 0; k < 4; ++k) hl ^= seg_hash(v[k], jg0 + (uint64_t)k * kSegStrideG);
+                tacc = finish_block(hl, gblk, h, lane, check, want);
             }
-            for (uint32_t i = 0; i < mine; i += kDepth) {
-#pragma unroll
-                for (int d = 0; d < kDepth; ++d) {
-                    const uint32_t ii = i + d;
-                    if (ii >= mine) break;
-                    const uint32_t b = wave + ii * kWaves;
-                    if (OP != kVerify) store_block(ring[d], dst + (size_t)b * kBlockBytes);
-                    if (HASH) {
-                        const uint64_t jg0 = jg_chunk + (uint64_t)b * kBlockStrideG;
-                        uint64_t hl = 0;
-#pragma unroll
-                        for (int k = 0; k < 4; ++k) hl ^= seg_hash(ring[d][k], jg0 + (uint64_t)k * kSegStrideG);
-                        tacc ^= finish_block(hl, g0 + b, h, lane, check, want[d]);
-                    }
-                    if (ii + kDepth < mine) {
-                        const uint32_t nb = b + kDepth * kWaves;
-                        if (HASH) want[d] = *(check ? h.expected + g0 + nb : exp_dummy);
-                        load_block(ring[d], src + (size_t)nb * kBlockBytes);
-                    }
-                }
-            }
-        }
-
-        // ---- phase 2: ragged last block and/or unaligned entry
-        for (uint32_t b = nfull + wave; b < nblk; b += kWaves) {
+        } else if (b < nblk) {  // ragged last block, or a block of an unaligned entry
             const uint32_t boff = b * kBlockBytes;
-            const uint64_t jg0 = jg_chunk + (uint64_t)b * kBlockStrideG;
             uint64_t hl = 0;
 #pragma unroll
             for (int k = 0; k < 4; ++k) {
@@ -267,11 +230,11 @@ k_stream(const Chunk *__restrict__ chunks, uint64_t count, gbyte *__restrict__ i
                 const uint32_t valid = p >= c.len ? 0u : min(16u, c.len - p);
                 u32x4 v;
                 if (OP == kRestore) {
-                    v = keep_bytes(*(const gvec *)(img + boff + k * 1024), valid);
-                    store_part(ent + boff + k * 1024, v, valid, aligned);
+                    v = keep_bytes(*(const gvec *)(img + k * 1024), valid);
+                    store_part(ent + k * 1024, v, valid, aligned);
                 } else {
-                    v = load_part(ent + boff + k * 1024, valid, aligned);
-                    if (OP == kSnapshot) *(gvec *)(img + boff + k * 1024) = v;
+                    v = load_part(ent + k * 1024, valid, aligned);
+                    if (OP == kSnapshot) *(gvec *)(img + k * 1024) = v;
                 }
                 if (HASH) {
                     const uint64_t jg = jg0 + (uint64_t)k * kSegStrideG;
@@ -281,10 +244,10 @@ k_stream(const Chunk *__restrict__ chunks, uint64_t count, gbyte *__restrict__ i
                     if (valid > 8) hl ^= mix64(w1 ^ (jg + kG));
                 }
             }
-            if (HASH) tacc ^= finish_block(hl, g0 + b, h, lane, check, check ? h.expected[g0 + b] : 0);
+            if (HASH) tacc = finish_block(hl, gblk, h, lane, check, check ? h.expected[gblk] : 0);
         }
 
-        // ---- tensor hash: XOR of the eight waves' partials, one atomic per chunk
+        // ---- tensor hash: XOR of the workgroup's block hashes, one atomic per unit
         if (HASH && h.ten) {
             if (lane == 0) wave_part[wave] = tacc;
             __syncthreads();
@@ -299,7 +262,7 @@ k_stream(const Chunk *__restrict__ chunks, uint64_t count, gbyte *__restrict__ i
     }
 }
 
-__global__ void __launch_bounds__(kThreads)
+__global__ void __launch_bounds__(kUnitThreads)
 k_prologue(uint64_t *__restrict__ ten, uint64_t n, uint64_t *__restrict__ mm_count)
 {
     const uint64_t tid = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x;
@@ -309,35 +272,24 @@ k_prologue(uint64_t *__restrict__ ten, uint64_t n, uint64_t *__restrict__ mm_cou
     if (mm_count && tid == 0) *mm_count = 0;
 }
 
-constexpr uint64_t kMaxGrid = 1u << 20;  // a multiple of kXcds
-// Dynamic LDS per workgroup: restore and snapshot ask for more than half of a
-// CU's 160 KiB so that one 8-wave workgroup is resident per CU; verify
-// (read-only) only needs the wave partials and runs at full occupancy.
-constexpr size_t kLdsCopy = 96 * 1024;
+constexpr uint64_t kMaxGrid = 1ull << 30;  // a multiple of kXcds
+// Dynamic LDS per workgroup: restore and snapshot ask for a sixth of a CU's
+// 160 KiB so that six 2-wave workgroups are resident per CU; verify
+// (read-only, heavier on VALU per byte) only needs the wave partials and runs
+// at full occupancy.
+constexpr size_t kLdsCopy = 26 * 1024;
 constexpr size_t kLdsVerify = kWaves * sizeof(uint64_t);
-constexpr int kMaxDevices = 64;
 
 template <int OP, bool HASH>
-hipError_t launch_t(const Chunk *chunks, uint64_t first, uint64_t count, uint8_t *img_base,
+hipError_t launch_t(const Chunk *chunks, uint64_t first, uint64_t count, uint32_t unit_shift, uint8_t *img_base,
                     uint64_t img_origin, const HashOut &h, hipStream_t s)
 {
     constexpr size_t lds = OP == kVerify ? kLdsVerify : kLdsCopy;
-    if (lds > 64 * 1024) {  // opt in to more than 64 KiB of dynamic LDS, once per device
-        static std::once_flag attr_once[kMaxDevices];
-        static hipError_t attr_err[kMaxDevices];
-        int dev = 0;
-        hipError_t e = hipGetDevice(&dev);
-        if (e != hipSuccess) return e;
-        if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
-        std::call_once(attr_once[dev], [dev] {
-            attr_err[dev] = hipFuncSetAttribute((const void *)k_stream<OP, HASH>,
-                                                hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
-        });
-        if (attr_err[dev] != hipSuccess) return attr_err[dev];
-    }
-    const uint64_t grid = ((count < kMaxGrid ? count : kMaxGrid) + kXcds - 1) / kXcds * kXcds;
-    hipLaunchKernelGGL((k_stream<OP, HASH>), dim3((uint32_t)grid), dim3(kThreads), lds, s, chunks + first, count,
-                       (gbyte *)img_base, img_origin, h);
+    static_assert(lds <= 64 * 1024, "above 64 KiB the launch would have to opt in per device");
+    const uint64_t units = count << unit_shift;
+    const uint64_t grid = ((units < kMaxGrid ? units : kMaxGrid) + kXcds - 1) / kXcds * kXcds;
+    hipLaunchKernelGGL((k_stream<OP, HASH>), dim3((uint32_t)grid), dim3(kUnitThreads), lds, s, chunks + first, count,
+                       unit_shift, (gbyte *)img_base, img_origin, h);
     return hipGetLastError();
 }
 
@@ -349,23 +301,29 @@ hipError_t launch_prologue(const HashOut &h, uint64_t n_entries, hipStream_t s)
     uint64_t *cnt = h.expected ? h.mm_count : nullptr;
     if (!ten && !cnt) return hipSuccess;
     uint64_t items = ten ? n_entries : 1;
-    uint64_t grid = (items + kThreads - 1) / kThreads;
+    uint64_t grid = (items + kUnitThreads - 1) / kUnitThreads;
     if (grid == 0) grid = 1;
     if (grid > 4096) grid = 4096;
-    hipLaunchKernelGGL(k_prologue, dim3((uint32_t)grid), dim3(kThreads), 0, s, ten, ten ? n_entries : 0, cnt);
+    hipLaunchKernelGGL(k_prologue, dim3((uint32_t)grid), dim3(kUnitThreads), 0, s, ten, ten ? n_entries : 0, cnt);
     return hipGetLastError();
 }
 
 hipError_t launch_stream(int op, bool hash, const Chunk *chunks, uint64_t first, uint64_t count,
-                         uint8_t *img_base, uint64_t img_origin, const HashOut &h, hipStream_t s)
+                         uint64_t chunk_bytes, uint8_t *img_base, uint64_t img_origin, const HashOut &h,
+                         hipStream_t s)
 {
     if (count == 0) return hipSuccess;
+    // 2^shift units of kWaves blocks cover a chunk
+    const uint64_t units_per_chunk = (chunk_bytes + kWaves * kBlockBytes - 1) / (kWaves * kBlockBytes);
+    uint32_t shift = 0;
+    while ((1ull << shift) < units_per_chunk) ++shift;
+    if ((count << shift) >> shift != count) return hipErrorInvalidValue;
     switch (op * 2 + (hash ? 1 : 0)) {
-    case kRestore * 2: return launch_t<kRestore, false>(chunks, first, count, img_base, img_origin, h, s);
-    case kRestore * 2 + 1: return launch_t<kRestore, true>(chunks, first, count, img_base, img_origin, h, s);
-    case kSnapshot * 2: return launch_t<kSnapshot, false>(chunks, first, count, img_base, img_origin, h, s);
-    case kSnapshot * 2 + 1: return launch_t<kSnapshot, true>(chunks, first, count, img_base, img_origin, h, s);
-    case kVerify * 2 + 1: return launch_t<kVerify, true>(chunks, first, count, img_base, img_origin, h, s);
+    case kRestore * 2: return launch_t<kRestore, false>(chunks, first, count, shift, img_base, img_origin, h, s);
+    case kRestore * 2 + 1: return launch_t<kRestore, true>(chunks, first, count, shift, img_base, img_origin, h, s);
+    case kSnapshot * 2: return launch_t<kSnapshot, false>(chunks, first, count, shift, img_base, img_origin, h, s);
+    case kSnapshot * 2 + 1: return launch_t<kSnapshot, true>(chunks, first, count, shift, img_base, img_origin, h, s);
+    case kVerify * 2 + 1: return launch_t<kVerify, true>(chunks, first, count, shift, img_base, img_origin, h, s);
     default: return hipErrorInvalidValue;
     }
 }
