@@ -133,6 +133,21 @@ def test_ragged_manifest_device(seed, aligned):
     _round_trip(arena, datas, gms.MEM_DEVICE, chunk_bytes=int(rng.choice([0, 4096, 12288, 1 << 20])))
 
 
+@pytest.mark.parametrize("chunk_kib", [4, 8, 20, 36, 64, 196, 64 * 1024])
+def test_chunk_geometries(chunk_kib):
+    """Chunk sizes whose block counts split unevenly into the kernel's work units (a unit's
+    second block past the chunk's end), up to the 64 MiB maximum, with ragged and unaligned
+    entries: snapshot, restore and verify all equal the oracle."""
+    need_gpu()
+    rng = np.random.default_rng(700 + chunk_kib)
+    sizes = [int(v) for v in rng.integers(1, 90_000, 12)] + [(5 << 20) + 4099, 0, 4096 * 9, 17, (chunk_kib << 10) + 1]
+    misalign = [0 if i % 3 else int(rng.integers(1, 16)) for i in range(len(sizes))]
+    arena = Arena(sizes, misalign=misalign, seed=chunk_kib)
+    datas = random_datas(sizes, seed=chunk_kib + 1)
+    arena.fill(datas)
+    _round_trip(arena, datas, gms.MEM_DEVICE, chunk_bytes=chunk_kib << 10)
+
+
 @pytest.mark.parametrize("staging", [None, (256 * 1024, 2), (1 << 20, 3), (0, 0)],
                          ids=["ring_default", "ring_256k_x2", "ring_1m_x3", "zero_copy"])
 def test_ragged_manifest_pinned(staging):
