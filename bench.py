@@ -29,7 +29,8 @@ sys.path.insert(0, ROOT)
 
 METRIC = "restore+verify GB/s on 1 GPU; seconds to restore a 16 GB weight shard"
 HBM_PEAK_GBS = 8000.0
-ALL_ROWS = ["main", "snapshot", "plain", "verify", "h2d", "file", "kv", "kv_vmm", "copy", "cpu", "shards"]
+ALL_ROWS = ["main", "snapshot", "plain", "verify", "sequential", "tiny", "h2d", "file", "kv", "kv_vmm", "copy", "cpu",
+            "shards"]
 # What shapes the measured kernel's accesses: the kernel and its launch code, the
 # header's constants (block and default chunk size) and the chunking in manifest creation.
 KERNEL_SOURCES = ["paper_2609_25451_amd/csrc/gms_kernels.hip", "paper_2609_25451_amd/csrc/gms_internal.h"]
@@ -122,7 +123,9 @@ def main():
     # ---------------------------------------------------------------- workload
     t0 = time.time()
     seed, specs, tensors = build_weights(torch, synth, "llama8b")
+    tm = time.perf_counter()
     m = gms.Manifest(tensors, device=0)
+    manifest_s = time.perf_counter() - tm
     P, nb, n, nchunks = m.payload_bytes, m.num_blocks, m.num_entries, m.num_chunks
     image = torch.empty(m.image_bytes, dtype=torch.uint8, device="cuda")
     expected = torch.zeros(nb, dtype=torch.int64, device="cuda")
@@ -190,6 +193,20 @@ def main():
         assert int(vc.item()) == 0
         t = statistics.median(ts)
         result_rows["verify_only"] = {"s": t, "GB_s": P / t / 1e9, "hbm_frac": P / t / 1e9 / HBM_PEAK_GBS}
+    if "sequential" in rows:  # restore, then a separate verify pass: 3P bytes against the fused 2P
+        vc = torch.zeros(1, dtype=torch.int64, device="cuda")
+
+        def seq():
+            gms.restore(m, image, m.image_bytes, gms.MEM_DEVICE)
+            gms.verify(m, expected=expected, mismatch_count=vc)
+
+        t = statistics.median(timer.run(seq, 5))
+        assert int(vc.item()) == 0
+        result_rows["restore_then_verify_sequential"] = {
+            "s": t, "GB_s": P / t / 1e9, "hbm_frac": (3 * P + 8 * nb) / t / 1e9 / HBM_PEAK_GBS,
+            "fused_speedup": t / statistics.median(main_times) if main_times else None}
+    if "tiny" in rows:
+        result_rows["tiny"] = bench_tiny(torch, gms, synth, timer)
     if "copy" in rows:
         a = torch.empty(4 << 30, dtype=torch.uint8, device="cuda")
         b = torch.empty_like(a)
@@ -206,9 +223,10 @@ def main():
         del a, b
 
     if "h2d" in rows:
-        t0 = time.time()
+        t0 = time.perf_counter()
         pinned = torch.empty(m.image_bytes, dtype=torch.uint8, pin_memory=True)
-        log(f"pinned {m.image_bytes} B in {time.time() - t0:.1f}s")
+        pin_s = time.perf_counter() - t0
+        log(f"pinned {m.image_bytes} B in {pin_s:.1f}s")
         # link peak: 1 GiB pinned -> device copies
         gib = pinned[: 1 << 30]
         dst = torch.empty(1 << 30, dtype=torch.uint8, device="cuda")
@@ -232,6 +250,7 @@ def main():
         snap_z = statistics.median(timer.run(lambda: gms.snapshot(m, pinned, m.image_bytes, gms.MEM_HOST_PINNED), 2))
         m.set_staging(64 << 20, 4)
         result_rows["h2d"] = {
+            "pinned_alloc_s": pin_s,
             "link_peak_GB_s": link,
             "restore_verify_ring_s": th, "restore_verify_ring_GB_s": P / th / 1e9,
             "link_frac": P / th / 1e9 / link,
@@ -298,6 +317,7 @@ def main():
             "workload": "llama8b bf16 weight set: 32 layers, d_model 4096, GQA 32q/8kv x 128, SwiGLU ffn 14336, "
                         "vocab 128256; 291 tensors; device-resident image; fused restore+verify",
             "payload_bytes": P, "entries": n, "blocks": nb, "chunks": nchunks, "block_bytes": 4096,
+            "manifest_create_s": round(manifest_s, 4),
         },
         "seconds_to_restore_16GB": {
             "device_image_restore_verify": round(statistics.mean(main_times), 6) if main_times else None,
@@ -389,6 +409,46 @@ def raw_direct_read(path, nbytes, threads=16, piece=16 << 20):
         return nbytes / (time.perf_counter() - t0)
     finally:
         os.close(fd)
+
+
+def bench_tiny(torch, gms, synth, timer):
+    """The tiny 21-tensor set (8.4 MB): it fits in the 256 MB last-level cache, so it is
+    reported as latency, not against the HBM roofline."""
+    seed, specs, tensors = build_weights(torch, synth, "tiny")
+    m = gms.Manifest(tensors, device=0)
+    img = torch.empty(m.image_bytes, dtype=torch.uint8, device="cuda")
+    exp = torch.zeros(m.num_blocks, dtype=torch.int64, device="cuda")
+    gms.snapshot(m, img, m.image_bytes, blk_hash=exp)
+    cnt = torch.zeros(1, dtype=torch.int64, device="cuda")
+    fused = lambda: gms.restore(m, img, m.image_bytes, expected=exp, mismatch_count=cnt)
+    for _ in range(3):
+        fused()
+    t = statistics.median(timer.run(fused, 20))
+    assert int(cnt.item()) == 0
+    ts = statistics.median(timer.run(lambda: gms.snapshot(m, img, m.image_bytes, blk_hash=exp), 20))
+    out = {"tensors": len(tensors), "payload_bytes": m.payload_bytes, "restore_verify_us": round(t * 1e6, 1),
+           "snapshot_us": round(ts * 1e6, 1)}
+    m.close()
+    return out
+
+
+def host_info():
+    """CPU model, cores available to this process and NUMA nodes of the measuring host."""
+    model = ""
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    nodes = 0
+    try:
+        nodes = len([d for d in os.listdir("/sys/devices/system/node") if d.startswith("node") and d[4:].isdigit()])
+    except OSError:
+        pass
+    return {"cpu_model": model, "cores_available": len(os.sched_getaffinity(0)), "numa_nodes": nodes}
 
 
 def bench_kv(torch, np, gms, synth, timer):
@@ -550,7 +610,7 @@ def bench_cpu(torch, np, image, m, specs, sample_bytes=8 << 30):
             "sample": f"restore+verify (unpack + block-hash compare) of {k - k0} whole tensors of the llama8b set "
                       f"(tensors {k0}..{k - 1}, {total} B), {threads} threads over tensors, median of 5 passes",
             "seconds": round(tn, 3), "single_thread_value": round(total / t1 / 1e9, 4),
-            "single_thread_seconds": round(t1, 3)}
+            "single_thread_seconds": round(t1, 3), "host": host_info()}
 
 
 if __name__ == "__main__":
