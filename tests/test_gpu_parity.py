@@ -14,7 +14,7 @@ import torch
 import oracle
 import paper_2609_25451_amd as gms
 import synth
-from gpu_util import Arena, from_u64, host_bytes, need_gpu, random_datas, to_u64, u64_dev
+from gpu_util import SENTINEL, Arena, from_u64, host_bytes, need_gpu, random_datas, to_u64, u64_dev
 
 pytestmark = pytest.mark.gpu
 
@@ -146,6 +146,22 @@ def test_chunk_geometries(chunk_kib):
     datas = random_datas(sizes, seed=chunk_kib + 1)
     arena.fill(datas)
     _round_trip(arena, datas, gms.MEM_DEVICE, chunk_bytes=chunk_kib << 10)
+
+
+def test_many_tiny_entries():
+    """200,000 entries of 1 to 300 bytes at every alignment: every block takes the byte-granular
+    path and most of each chunk's work units are empty."""
+    need_gpu()
+    rng = np.random.default_rng(808)
+    sizes = [int(v) for v in rng.integers(1, 301, 200_000)]
+    sizes[::1000] = [0] * len(sizes[::1000])
+    arena = Arena(sizes, misalign=lambda r: r.integers(0, 16), gap=8, seed=8)
+    datas = [synth.random_bytes(n, 88, i) for i, n in enumerate(sizes)]
+    host = np.full(arena.total, SENTINEL, dtype=np.uint8)
+    for o, d in zip(arena.offsets, datas):
+        host[o:o + d.size] = d
+    arena.buf.copy_(torch.from_numpy(host))
+    _round_trip(arena, datas, gms.MEM_DEVICE)
 
 
 @pytest.mark.parametrize("staging", [None, (256 * 1024, 2), (1 << 20, 3), (0, 0)],
