@@ -216,7 +216,10 @@ enum gms_file_flags {
  * and enqueued; device work completes on `stream`.  The first file call
  * allocates the manifest's pinned host ring: 2 x slots (at most 16) slices.
  * Errors: as gms_restore, plus GMS_ERR_IO (open/read failure) and
- * GMS_ERR_SIZE (file shorter than file_offset + gms_image_bytes).
+ * GMS_ERR_SIZE (file shorter than file_offset + gms_image_bytes).  After an
+ * I/O error, slices already read may have been restored (and counted in the
+ * hash outputs): the entries and outputs are then partial and must not be
+ * used; the manifest stays usable.
  */
 int gms_restore_from_file(const gms_manifest *m, const char *path, uint64_t file_offset, uint32_t flags,
                           uint32_t io_threads, const uint64_t *expected_blk, uint64_t *blk_hash_out,

@@ -385,6 +385,8 @@ class Store:
         return int(cnt.value)
 
     def layout(self) -> Manifest | None:
+        """The committed layout, as a manifest owned by the store: valid until the next writer
+        connects or the store is closed."""
         h = _store_layout(self._h)
         return Manifest._borrow(h, self) if h else None
 
@@ -398,11 +400,20 @@ class _Lease:
         self.id = lease
         self.open = True
 
+    def _handle(self):
+        h = getattr(self.store, "_h", None)
+        if h is None or not h.value:
+            raise GmsError(GMS_ERR_STATE, "lease of a closed store")
+        return h
+
     def close(self) -> None:
-        """Ends the lease (a writer's before commit discards its state)."""
+        """Ends the lease (a writer's before commit discards its state); a no-op once the
+        store itself is closed, which ended every lease."""
         if self.open:
             self.open = False
-            _check(_store_disconnect(self.store._h, self.id), "gms_store_disconnect")
+            h = getattr(self.store, "_h", None)
+            if h is not None and h.value:
+                _check(_store_disconnect(h, self.id), "gms_store_disconnect")
 
     def __enter__(self):
         return self
@@ -416,16 +427,16 @@ class WriteLease(_Lease):
 
     def alloc(self, nbytes: int, align: int = 0) -> int:
         out = U64()
-        _check(_store_alloc(self.store._h, self.id, nbytes, align, ctypes.byref(out)), "gms_store_alloc")
+        _check(_store_alloc(self._handle(), self.id, nbytes, align, ctypes.byref(out)), "gms_store_alloc")
         return int(out.value)
 
     def free(self, addr: int) -> None:
-        _check(_store_free(self.store._h, self.id, addr), "gms_store_free")
+        _check(_store_free(self._handle(), self.id, addr), "gms_store_free")
 
     def commit(self, entries, expected=None, stream=None) -> None:
         ranges = _ranges(entries)
         cnt = U64()
-        rc = _store_commit(self.store._h, self.id, _entry_array(ranges), len(ranges), _ptr(expected),
+        rc = _store_commit(self._handle(), self.id, _entry_array(ranges), len(ranges), _ptr(expected),
                            ctypes.byref(cnt), _stream(stream))
         if rc != GMS_OK:
             raise GmsError(rc, "gms_store_commit", int(cnt.value))
@@ -434,7 +445,7 @@ class WriteLease(_Lease):
     def abort(self) -> None:
         if self.open:
             self.open = False
-            _check(_store_abort(self.store._h, self.id), "gms_store_abort")
+            _check(_store_abort(self._handle(), self.id), "gms_store_abort")
 
 
 class ReadLease(_Lease):

@@ -202,3 +202,14 @@ def test_concurrent_readers_and_python_leases():
             w.commit([(0x1000, 16)])
         assert e.value.status == gms.GMS_ERR_STATE
     s.close()
+
+
+def test_leases_outlive_a_closed_store():
+    s = gms.Store(device=gms.HOST_ONLY)
+    w = s.connect_rw()
+    s.close()
+    w.close()  # the store ended every lease when it closed: nothing left to release
+    w2 = gms.WriteLease(s, 1)
+    with pytest.raises(gms.GmsError) as e:
+        w2.commit([])
+    assert e.value.status == gms.GMS_ERR_STATE
