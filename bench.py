@@ -265,8 +265,9 @@ def main():
     if "file" in rows:
         result_rows["file"] = bench_file(torch, gms, m, expected)
 
+    link = result_rows.get("h2d", {}).get("link_peak_GB_s")
     if "kv" in rows:
-        result_rows["kv_pool"] = bench_kv(torch, np, gms, synth, timer)
+        result_rows["kv_pool"] = bench_kv(torch, np, gms, synth, timer, link)
     if "kv_vmm" in rows:
         result_rows["kv_pool_vmm"] = bench_kv_vmm(torch, np, gms, synth, timer)
 
@@ -297,7 +298,8 @@ def main():
         m.close()
         torch.cuda.synchronize()
         torch.cuda.empty_cache()
-        result_rows["shards"] = {name: bench_shard(torch, gms, synth, timer, name) for name in ("llama70b_tp8", "moe")}
+        result_rows["shards"] = {name: bench_shard(torch, gms, synth, timer, name, link)
+                                 for name in ("llama70b_tp8", "moe")}
 
     value = P * args.steps / wall / 1e9 if main_times else None
     out = {
@@ -451,7 +453,7 @@ def host_info():
     return {"cpu_model": model, "cores_available": len(os.sched_getaffinity(0)), "numa_nodes": nodes}
 
 
-def bench_kv(torch, np, gms, synth, timer):
+def bench_kv(torch, np, gms, synth, timer, link=None):
     """8 GiB paged KV pool: restore only the live blocks + verify, one planted bit flip."""
     p = synth.kv_pool()
     pool = [torch.empty(p.layer_bytes, dtype=torch.uint8, device="cuda") for _ in range(p.layers)]
@@ -486,12 +488,41 @@ def bench_kv(torch, np, gms, synth, timer):
     dead = np.setdiff1d(np.arange(p.blocks), live)
     dead_ok = all(bool((t.view(p.blocks, p.unit_bytes)[torch.from_numpy(dead).cuda()] == 0xA5).all()) for t in pool[:4])
     t = statistics.median(ts)
+    h2d = h2d_leg(torch, gms, timer, m, img, exp, link)  # the same planted flip, through the host link
     return {"entries": m.num_entries, "payload_bytes": P, "s": t, "GB_s": P / t / 1e9,
             "hbm_frac": 2 * P / t / 1e9 / HBM_PEAK_GBS, "mismatches": c, "flagged": flagged,
-            "planted_block": int(base[e] + blk), "dead_units_untouched_first4_layers": dead_ok}
+            "planted_block": int(base[e] + blk), "dead_units_untouched_first4_layers": dead_ok, "h2d": h2d}
 
 
-def bench_shard(torch, gms, synth, timer, name):
+H2D_MAX_PINNED = 64 << 30  # the measuring host cannot pin the 122 GB MoE image
+
+
+def h2d_leg(torch, gms, timer, m, img, exp, link=None, reps=3, cap=8):
+    """The same restore+verify from a pinned host copy of the image, through the staging ring:
+    pinning time (not timed in the rate), rate, and the mismatches it reports.  One untimed
+    call first allocates the manifest's staging ring."""
+    if m.image_bytes > H2D_MAX_PINNED:
+        return {"skipped": f"image of {m.image_bytes} B is above the {H2D_MAX_PINNED} B this host can pin"}
+    t0 = time.perf_counter()
+    pinned = torch.empty(m.image_bytes, dtype=torch.uint8, pin_memory=True)
+    pin_s = time.perf_counter() - t0
+    pinned.copy_(img)
+    cnt = torch.zeros(1, dtype=torch.int64, device="cuda")
+    lst = torch.zeros(cap, dtype=torch.int64, device="cuda")
+    run = lambda: gms.restore(m, pinned, m.image_bytes, gms.MEM_HOST_PINNED, expected=exp, mismatch_count=cnt,
+                              mismatch_list=lst, mismatch_cap=cap)
+    run()
+    t = statistics.median(timer.run(run, reps))
+    c = int(cnt.item())
+    out = {"pinned_alloc_s": round(pin_s, 3), "restore_verify_s": t, "restore_verify_GB_s": m.payload_bytes / t / 1e9,
+           "mismatches": c, "flagged": sorted(int(v) for v in lst[:min(c, cap)].cpu().tolist())}
+    if link:
+        out["link_frac"] = m.payload_bytes / t / 1e9 / link
+    del pinned
+    return out
+
+
+def bench_shard(torch, gms, synth, timer, name, link=None):
     """Fused restore+verify of another weight workload from a device-resident image."""
     _, specs = synth.weight_set(name)
     P = sum(sp.nbytes for sp in specs)
@@ -510,6 +541,10 @@ def bench_shard(torch, gms, synth, timer, name):
     out = {"tensors": len(tensors), "payload_bytes": P, "chunks": m.num_chunks, "restore_verify_s": t,
            "restore_verify_GB_s": P / t / 1e9, "hbm_frac": (2 * P + 8 * m.num_blocks) / t / 1e9 / HBM_PEAK_GBS}
     log(f"{name}: restore+verify {t * 1e3:.2f} ms, {out['hbm_frac'] * 100:.1f}% of HBM peak")
+    out["h2d"] = h2d_leg(torch, gms, timer, m, img, exp, link)
+    if "skipped" not in out["h2d"]:
+        assert out["h2d"]["mismatches"] == 0
+        log(f"{name}: H2D restore+verify {out['h2d']['restore_verify_s']:.3f} s")
     m.close()
     del tensors, img, exp
     torch.cuda.synchronize()
