@@ -29,8 +29,8 @@ sys.path.insert(0, ROOT)
 
 METRIC = "restore+verify GB/s on 1 GPU; seconds to restore a 16 GB weight shard"
 HBM_PEAK_GBS = 8000.0
-ALL_ROWS = ["main", "snapshot", "plain", "verify", "sequential", "tiny", "h2d", "file", "kv", "kv_vmm", "copy", "cpu",
-            "shards"]
+ALL_ROWS = ["main", "snapshot", "plain", "verify", "sequential", "tiny", "h2d", "file", "kv", "kv_vmm", "store", "copy",
+            "cpu", "shards"]
 # What shapes the measured kernel's accesses: the kernel and its launch code, the
 # header's constants (block and default chunk size) and the chunking in manifest creation.
 KERNEL_SOURCES = ["paper_2609_25451_amd/csrc/gms_kernels.hip", "paper_2609_25451_amd/csrc/gms_internal.h"]
@@ -270,6 +270,8 @@ def main():
         result_rows["kv_pool"] = bench_kv(torch, np, gms, synth, timer, link)
     if "kv_vmm" in rows:
         result_rows["kv_pool_vmm"] = bench_kv_vmm(torch, np, gms, synth, timer)
+    if "store" in rows:
+        result_rows["store"] = bench_store(torch, gms, m, image, expected)
 
     # ---------------------------------------------------------------- roofline
     roof = None
@@ -550,6 +552,48 @@ def bench_shard(torch, gms, synth, timer, name, link=None):
     torch.cuda.synchronize()
     torch.cuda.empty_cache()
     return out
+
+
+def bench_store(torch, gms, m, image, expected):
+    """The lease protocol on the llama8b set in a store of its own: a writer populates the
+    store's allocations from the device image with a fused restore+verify and commits them
+    (hashing every block, mapping the pool read-only); a replacement then attaches read-only
+    after re-hashing the committed state.  Wall times of the synchronous calls."""
+    sizes = list(m.sizes)
+    P = m.payload_bytes
+    store = gms.Store(va_bytes=P + (8 << 30), slab_bytes=2 << 30)
+    try:
+        w = store.connect_rw()
+        addrs = [w.alloc(n) for n in sizes]
+        sm = gms.Manifest(list(zip(addrs, sizes)), device=0)
+        cnt = torch.zeros(1, dtype=torch.int64, device="cuda")
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        gms.restore(sm, image, sm.image_bytes, expected=expected, mismatch_count=cnt)
+        torch.cuda.synchronize()
+        populate = time.perf_counter() - t0
+        assert int(cnt.item()) == 0
+        t0 = time.perf_counter()
+        w.commit(list(zip(addrs, sizes)), expected=expected)
+        commit = time.perf_counter() - t0
+        attach = []
+        for _ in range(5):
+            t0 = time.perf_counter()
+            r = store.connect_ro(verify=True)
+            attach.append(time.perf_counter() - t0)
+            r.close()
+        t0 = time.perf_counter()
+        w2 = store.connect_rw()  # the writer reacquires: the pool becomes writable again
+        reacquire = time.perf_counter() - t0
+        w2.commit(list(zip(addrs, sizes)))
+        sm.close()
+        out = {"payload_bytes": P, "populate_restore_verify_s": populate, "commit_s": commit,
+               "attach_ro_verified_s": statistics.median(attach), "writer_reacquire_s": reacquire,
+               "mappings": store.pool_info()["mappings"]}
+        log(f"store: commit {commit * 1e3:.1f} ms, verified read-only attach {out['attach_ro_verified_s'] * 1e3:.2f} ms")
+        return out
+    finally:
+        store.close()
 
 
 def bench_kv_vmm(torch, np, gms, synth, timer):
