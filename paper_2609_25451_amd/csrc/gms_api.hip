@@ -250,7 +250,7 @@ using gms::ensure_ring;
 // Device-resident image, or zero-copy access to a pinned one: one launch.
 int run_direct(const gms_manifest *m, int op, uint8_t *image, const HashOut &h, hipStream_t s)
 {
-    hipError_t e = gms::launch_stream(op, h.any(), m->d_chunks, 0, m->chunks.size(), m->chunk_bytes, image, 0, h, s);
+    hipError_t e = gms::launch_stream(op, h.any(), m->d_chunks, 0, m->chunks.size(), m->max_chunk, image, 0, h, s);
     return e == hipSuccess ? GMS_OK : fail_hip(e, "kernel launch");
 }
 
@@ -287,7 +287,7 @@ int run_ring(gms_manifest *m, const HashOut &h, uint8_t *host_image, hipStream_t
         GMS_TRY(hipMemcpyAsync(dev, host_image + lo, bytes, hipMemcpyHostToDevice, m->copy_stream));
         GMS_TRY(hipEventRecord(m->ev_filled[slot], m->copy_stream));
         GMS_TRY(hipStreamWaitEvent(s, m->ev_filled[slot], 0));
-        GMS_TRY(gms::launch_stream(gms::kRestore, h.any(), m->d_chunks, c0, c1 - c0, m->chunk_bytes, dev, lo, h, s));
+        GMS_TRY(gms::launch_stream(gms::kRestore, h.any(), m->d_chunks, c0, c1 - c0, m->max_chunk, dev, lo, h, s));
         GMS_TRY(hipEventRecord(m->ev_free[slot], s));
     }
     GMS_TRY(hipEventRecord(m->ev_done, s));
@@ -431,6 +431,7 @@ int gms_manifest_create(const gms_entry *entries, uint64_t n, int device, uint64
                 c.len = (uint32_t)len;
                 c.entry = (uint32_t)i;
                 m->chunks.push_back(c);
+                m->max_chunk = std::max(m->max_chunk, len);
                 pos += len;
             }
             off += ceil_div(nb, GMS_BLOCK_BYTES) * GMS_BLOCK_BYTES;

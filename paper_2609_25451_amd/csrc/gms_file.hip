@@ -327,7 +327,7 @@ int gms_restore_from_file(const gms_manifest *cm, const char *path, uint64_t fil
             (e = hipEventRecord(m->ev_filled[slot], m->copy_stream)) != hipSuccess ||
             (e = hipStreamWaitEvent(s, m->ev_filled[slot], 0)) != hipSuccess ||
             (e = gms::launch_stream(gms::kRestore, h.any(), m->d_chunks, m->slice_first[sl],
-                                    m->slice_first[sl + 1] - m->slice_first[sl], m->chunk_bytes, dev, lo, h, s)) !=
+                                    m->slice_first[sl + 1] - m->slice_first[sl], m->max_chunk, dev, lo, h, s)) !=
                 hipSuccess ||
             (e = hipEventRecord(m->ev_free[slot], s)) != hipSuccess) {
             rc = fail_hip(e, "file restore slice");
@@ -378,7 +378,7 @@ int gms_snapshot_to_file(const gms_manifest *cm, const char *path, uint32_t flag
     auto enqueue = [&](uint64_t sl) -> int {
         const uint32_t hslot = (uint32_t)(sl % hk);
         const uint64_t c0 = m->slice_first[sl], c1 = m->slice_first[sl + 1];
-        GMS_TRY(gms::launch_stream(gms::kSnapshot, h.any(), m->d_chunks, c0, c1 - c0, m->chunk_bytes,
+        GMS_TRY(gms::launch_stream(gms::kSnapshot, h.any(), m->d_chunks, c0, c1 - c0, m->max_chunk,
                                    h_dev + (uint64_t)hslot * slice, sl * slice, h, s));
         GMS_TRY(hipEventRecord(m->ev_host[hslot], s));
         return GMS_OK;

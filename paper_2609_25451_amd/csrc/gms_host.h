@@ -48,6 +48,7 @@ struct gms_manifest {
     int device = GMS_HOST_ONLY;
     uint64_t n = 0;
     uint64_t chunk_bytes = 0;
+    uint64_t max_chunk = 0;  // longest chunk: sizes the kernel's work units
     uint64_t payload = 0, image_bytes = 0, num_blocks = 0;
     std::vector<uint64_t> img_off;
     std::vector<gms::Chunk> chunks;  // host copy, sorted by image offset
