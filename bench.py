@@ -43,17 +43,26 @@ def log(*a):
     print("[bench]", *a, file=sys.stderr, flush=True)
 
 
+def _code(text: str) -> str:
+    """C/C++ source without comments or blank lines (comments do not change a kernel)."""
+    import re
+
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    text = re.sub(r"//[^\n]*", "", text)
+    return "\n".join(l.rstrip() for l in text.splitlines() if l.strip())
+
+
 def kernel_source_digest() -> str:
     h = hashlib.sha256()
     for p in KERNEL_SOURCES:
-        with open(os.path.join(ROOT, p), "rb") as f:
-            h.update(f.read())
+        with open(os.path.join(ROOT, p)) as f:
+            h.update(_code(f.read()).encode())
     with open(os.path.join(ROOT, HEADER)) as f:
         h.update("".join(l for l in f if l.startswith("#define GMS_")).encode())
     with open(os.path.join(ROOT, CHUNKING[0])) as f:
         src = f.read()
     start = src.index(CHUNKING[1])
-    h.update(src[start:src.index("\n}\n", start)].encode())
+    h.update(_code(src[start:src.index("\n}\n", start)]).encode())
     return h.hexdigest()[:16]
 
 

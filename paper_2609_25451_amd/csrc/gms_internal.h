@@ -35,8 +35,8 @@ struct HashOut {
 // Zeroes the tensor-hash array and the mismatch counter (either may be null).
 hipError_t launch_prologue(const HashOut &h, uint64_t n_entries, hipStream_t s);
 
-// Runs `op` over chunks[first, first + count) of a manifest whose chunks are
-// at most `chunk_bytes` long.  The image byte at offset x lives at
+// Runs `op` over chunks[first, first + count), none longer than `chunk_bytes`
+// (the manifest's longest chunk sizes the kernel's work units).  The image byte at offset x lives at
 // img_base + (x - img_origin).  `hash` selects the hashing variant.
 hipError_t launch_stream(int op, bool hash, const Chunk *chunks, uint64_t first, uint64_t count,
                          uint64_t chunk_bytes, uint8_t *img_base, uint64_t img_origin, const HashOut &h,

@@ -163,13 +163,15 @@ __device__ __forceinline__ void store_block(const u32x4 v[4], gbyte *p)
     for (int k = 0; k < 4; ++k) __builtin_nontemporal_store(v[k], (gvec *)(p + k * 1024));
 }
 
+// Full 4 KiB blocks a chunk can move with 16-byte accesses: all of them when
+// its entry address is 16-byte aligned, none otherwise.
 __device__ __forceinline__ uint32_t fast_blocks(const Chunk &c)
 {
     return (c.addr & 15) == 0 ? c.len / kBlockBytes : 0;
 }
 
 // Unit u is blocks [(u mod 2^shift) * kWaves, +kWaves) of chunk u >> shift
-// (2^shift units cover the manifest's chunk size); wave w of the workgroup
+// (2^shift units cover the manifest's longest chunk); wave w of the workgroup
 // takes the unit's block w.  A full, aligned block is loaded with 16-byte
 // non-temporal loads, stored and hashed from the same registers; its expected
 // hash is loaded branch-free (a harmless address when not checking) just
