@@ -213,3 +213,76 @@ def test_leases_outlive_a_closed_store():
     with pytest.raises(gms.GmsError) as e:
         w2.commit([])
     assert e.value.status == gms.GMS_ERR_STATE
+
+
+# -- plausible mistakes in the reference model, each caught by the scenario pins ---------------
+
+class _RwWhileReaders(Model):
+    def connect_rw(self):
+        if self.state_name == "RO":
+            self.writer, self.state_name = self._lease(), "RW"
+            return "ok", self.writer
+        return super().connect_rw()
+
+
+class _LastReaderStaysRO(Model):
+    def disconnect(self, lease):
+        if lease in self.readers and len(self.readers) == 1:
+            self.readers.remove(lease)
+            return "ok"
+        return super().disconnect(lease)
+
+
+class _WriterLeaveKeepsState(Model):
+    def disconnect(self, lease):
+        if lease is not None and lease == self.writer:
+            return "ok"
+        return super().disconnect(lease)
+
+
+class _CommitKeepsWriter(Model):
+    def commit(self, lease):
+        w = self.writer
+        rc = super().commit(lease)
+        self.writer = w
+        return rc
+
+
+class _ReaderDuringWrite(Model):
+    def connect_ro(self):
+        if self.state_name == "RW":
+            lease = self._lease()
+            self.readers.add(lease)
+            return "ok", lease
+        return super().connect_ro()
+
+
+class _ReusedLeaseIds(Model):
+    def _lease(self):
+        return 1
+
+
+class _AbortToCommitted(Model):
+    def abort(self, lease):
+        rc = super().abort(lease)
+        if rc == "ok":
+            self.state_name = "COMMITTED"
+        return rc
+
+
+SCENARIOS = [test_cold_start_then_readers, test_writer_failure_before_commit_discards,
+             test_reader_failure_keeps_committed_state, test_exclusive_write_only_after_last_reader,
+             test_stale_and_foreign_leases]
+
+
+@pytest.mark.parametrize("mutant", [_RwWhileReaders, _LastReaderStaysRO, _WriterLeaveKeepsState, _CommitKeepsWriter,
+                                    _ReaderDuringWrite, _ReusedLeaseIds, _AbortToCommitted],
+                         ids=lambda c: c.__name__.lstrip("_"))
+def test_model_mutants_are_caught(mutant):
+    caught = []
+    for scenario in SCENARIOS:
+        try:
+            scenario(mutant())
+        except AssertionError:
+            caught.append(scenario.__name__)
+    assert caught, f"{mutant.__name__} passes every scenario pin"
