@@ -14,7 +14,7 @@ import torch
 import oracle
 import paper_2609_25451_amd as gms
 import synth
-from gpu_util import d2h, memset, need_gpu, to_u64, u64_dev
+from gpu_util import d2h, from_u64, memset, need_gpu, to_u64, u64_dev
 
 pytestmark = pytest.mark.gpu
 
@@ -186,4 +186,62 @@ def test_commit_rejects_ranges_outside_the_store():
             assert e.value.status == gms.GMS_ERR_INVALID
         w.commit([(a, 10_000), (a, 0)])
     assert s.state() == ("COMMITTED", 0, False)
+    s.close()
+
+
+def test_cold_repopulation_from_file(tmp_path):
+    """A cold store repopulated from storage by a separate writer, then attached read-only:
+    the weights are snapshotted to an image file with their block hashes; a writer lease
+    allocates the same layout in the store, streams the file into it (restore with verify),
+    commits against the file's hashes and a reader attaches after re-hashing.  A file with one
+    flipped byte is refused at commit with exactly one mismatching block."""
+    need_gpu()
+    seed, specs = synth.weight_set("tiny")
+    src = [torch.empty(sp.shape, dtype=torch.bfloat16, device="cuda") for sp in specs]
+    for i, t in enumerate(src):
+        synth.dev_fill_bf16(t.data_ptr(), t.numel(), seed, i)
+    datas = [synth.bf16_bits(sp.numel, seed, i).view(np.uint8) for i, sp in enumerate(specs)]
+    o_blk, _ = oracle.hashes(datas)
+    m0 = gms.Manifest(src)
+    path = tmp_path / "weights.img"
+    blk = u64_dev(m0.num_blocks)
+    gms.snapshot_to_file(m0, path, flags=gms.FILE_DIRECT | gms.FILE_SYNC, blk_hash=blk)
+    torch.cuda.synchronize()
+    assert np.array_equal(to_u64(blk, m0.num_blocks), o_blk)
+    sizes = [sp.nbytes for sp in specs]
+    m0.close()
+    del src
+
+    s = gms.Store(va_bytes=1 << 30, slab_bytes=SLAB)
+    w = s.connect_rw()
+    addrs = [w.alloc(n) for n in sizes]
+    m = gms.Manifest(list(zip(addrs, sizes)))
+    expected = from_u64(o_blk)
+    cnt = u64_dev(1)
+    gms.restore_from_file(m, path, flags=gms.FILE_DIRECT, expected=expected, mismatch_count=cnt)
+    torch.cuda.synchronize()
+    assert to_u64(cnt)[0] == 0
+    w.commit(list(zip(addrs, sizes)), expected=expected)
+    with s.connect_ro(verify=True):
+        assert np.array_equal(_store_hashes(s, s.layout()), o_blk)
+
+    # a damaged file: the writer's commit is refused, the store stays with the writer
+    img = np.fromfile(path, dtype=np.uint8)
+    off, _ = m.layout()
+    img[off[5] + 100] ^= 0x01
+    bad = tmp_path / "weights_bad.img"
+    img.tofile(bad)
+    w2 = s.connect_rw()
+    gms.restore_from_file(m, bad, flags=0, expected=expected, mismatch_count=cnt)
+    torch.cuda.synchronize()
+    assert to_u64(cnt)[0] == 1
+    with pytest.raises(gms.GmsError) as e:
+        w2.commit(list(zip(addrs, sizes)), expected=expected)
+    assert e.value.status == gms.GMS_ERR_INTEGRITY and e.value.mismatches == 1
+    assert s.state() == ("RW", 0, False)
+    gms.restore_from_file(m, path, expected=expected, mismatch_count=cnt)  # the good copy
+    torch.cuda.synchronize()
+    w2.commit(list(zip(addrs, sizes)), expected=expected)
+    assert s.state() == ("COMMITTED", 0, False)
+    m.close()
     s.close()
