@@ -148,6 +148,31 @@ def test_chunk_geometries(chunk_kib):
     _round_trip(arena, datas, gms.MEM_DEVICE, chunk_bytes=chunk_kib << 10)
 
 
+@pytest.mark.parametrize("seed", range(25))
+def test_random_manifests(seed):
+    """Seeded random manifests: entry counts, sizes (empty, a few bytes, around a block, several
+    MiB), alignments, chunk sizes and image kinds all drawn at random; snapshot, restore and
+    verify equal the oracle."""
+    need_gpu()
+    rng = np.random.default_rng(9000 + seed)
+    n = int(rng.integers(1, 61))
+    kinds = rng.choice(["zero", "tiny", "block", "mid", "big"], size=n, p=[0.1, 0.25, 0.3, 0.25, 0.1])
+    draw = {"zero": lambda: 0, "tiny": lambda: int(rng.integers(1, 64)),
+            "block": lambda: 4096 * int(rng.integers(1, 4)) + int(rng.integers(-3, 4)),
+            "mid": lambda: int(rng.integers(5000, 300_000)), "big": lambda: int(rng.integers(1 << 20, 6 << 20))}
+    sizes = [max(0, draw[k]()) for k in kinds]
+    arena = Arena(sizes, misalign=lambda r: r.integers(0, 16) if r.random() < 0.4 else 0, seed=seed)
+    datas = random_datas(sizes, seed=300 + seed)
+    arena.fill(datas)
+    chunk = 4096 * int(rng.choice([1, 2, 3, 5, 16, 17, 64, 256]))
+    mode = seed % 3
+    if mode == 0:
+        _round_trip(arena, datas, gms.MEM_DEVICE, chunk_bytes=chunk)
+    else:  # pinned host image through the staging ring (1) or zero-copy (2); default chunking
+        staging = (int(rng.choice([1, 2, 4])) << 20, int(rng.integers(1, 4))) if mode == 1 else (0, 0)
+        _round_trip(arena, datas, gms.MEM_HOST_PINNED, staging=staging)
+
+
 def test_many_tiny_entries():
     """200,000 entries of 1 to 300 bytes at every alignment: every block takes the byte-granular
     path and most of each chunk's work units are empty."""
