@@ -32,7 +32,7 @@ HBM_PEAK_GBS = 8000.0
 ALL_ROWS = ["main", "snapshot", "plain", "verify", "sequential", "tiny", "h2d", "file", "kv", "kv_vmm", "store", "copy",
             "cpu", "shards"]
 # What shapes the measured kernel's accesses: the kernel and its launch code, the
-# header's constants (block and default chunk size) and the chunking in manifest creation.
+# header's block and default chunk sizes and the chunking in manifest creation.
 KERNEL_SOURCES = ["paper_2609_25451_amd/csrc/gms_kernels.hip", "paper_2609_25451_amd/csrc/gms_internal.h"]
 HEADER = "include/gms.h"
 CHUNKING = ("paper_2609_25451_amd/csrc/gms_api.hip", "int gms_manifest_create(")
@@ -58,7 +58,8 @@ def kernel_source_digest() -> str:
         with open(os.path.join(ROOT, p)) as f:
             h.update(_code(f.read()).encode())
     with open(os.path.join(ROOT, HEADER)) as f:
-        h.update("".join(l for l in f if l.startswith("#define GMS_")).encode())
+        h.update("".join(l for l in f if l.startswith(("#define GMS_BLOCK_BYTES", "#define GMS_DEFAULT_CHUNK_BYTES")))
+                 .encode())
     with open(os.path.join(ROOT, CHUNKING[0])) as f:
         src = f.read()
     start = src.index(CHUNKING[1])
@@ -257,7 +258,7 @@ def main():
         tz = statistics.median(timer.run(h2d, 2))
         assert int(hc.item()) == 0
         snap_z = statistics.median(timer.run(lambda: gms.snapshot(m, pinned, m.image_bytes, gms.MEM_HOST_PINNED), 2))
-        m.set_staging(64 << 20, 4)
+        m.set_staging(gms.DEFAULT_SLICE_BYTES, gms.DEFAULT_SLOTS)
         result_rows["h2d"] = {
             "pinned_alloc_s": pin_s,
             "link_peak_GB_s": link,

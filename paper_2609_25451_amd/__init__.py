@@ -52,6 +52,8 @@ MEM_DEVICE = 0
 MEM_HOST_PINNED = 1
 HOST_ONLY = -1
 BLOCK_BYTES = 4096
+DEFAULT_SLICE_BYTES = 256 << 20  # GMS_DEFAULT_SLICE_BYTES
+DEFAULT_SLOTS = 2  # GMS_DEFAULT_SLOTS
 
 
 class GmsEntry(ctypes.Structure):

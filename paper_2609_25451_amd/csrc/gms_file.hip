@@ -3,7 +3,7 @@
 // A cold replacement repopulates model state from storage while the engine's
 // runtime is restored (paper section 3.3 and section 4, cold GMS repopulation);
 // the end-to-end cost is the artifact size over the effective bandwidth
-// (section 3.1).  Restore runs a three-stage pipeline per 64 MiB slice:
+// (section 3.1).  Restore runs a three-stage pipeline per staging slice:
 // parallel pread (O_DIRECT through per-worker bounce buffers when the file
 // system allows it, buffered otherwise) into a pinned host slot, a DMA of
 // that slot into a device slot on the manifest's copy stream, and the

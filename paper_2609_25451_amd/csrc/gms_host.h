@@ -14,8 +14,8 @@
 namespace gms {
 
 constexpr uint64_t kMaxChunk = 64ull << 20;
-constexpr uint64_t kDefaultSlice = 64ull << 20;
-constexpr uint32_t kDefaultSlots = 4;
+constexpr uint64_t kDefaultSlice = GMS_DEFAULT_SLICE_BYTES;
+constexpr uint32_t kDefaultSlots = GMS_DEFAULT_SLOTS;
 constexpr uint32_t kMaxSlots = 16;
 
 inline uint64_t ceil_div(uint64_t a, uint64_t b) { return a / b + (a % b != 0); }
