@@ -28,7 +28,7 @@ def _case(seed, misalign=True):
 
 
 @pytest.mark.parametrize("flags", [0, gms.FILE_DIRECT, gms.FILE_DIRECT | gms.FILE_SYNC])
-@pytest.mark.parametrize("staging", [None, (256 * 1024, 2), (1 << 20, 3)], ids=["ring64M", "ring256K", "ring1M"])
+@pytest.mark.parametrize("staging", [None, (256 * 1024, 2), (1 << 20, 3)], ids=["ring_default", "ring256K", "ring1M"])
 def test_file_round_trip(tmp_path, flags, staging):
     need_gpu()
     arena, datas = _case(1)
