@@ -17,3 +17,28 @@ def test_rows_listed_in_help():
     r = subprocess.run([sys.executable, os.path.join(ROOT, "bench.py"), "--help"], capture_output=True, text=True,
                        timeout=60)
     assert r.returncode == 0 and "kv_vmm" in r.stdout and "file" in r.stdout
+
+
+def test_traffic_digest_ignores_comments_but_not_code(tmp_path, monkeypatch):
+    """The stored traffic counts stay valid across comment edits and lapse on code edits."""
+    import shutil
+
+    import bench
+
+    for rel in bench.KERNEL_SOURCES + [bench.HEADER, bench.CHUNKING[0]]:
+        dst = tmp_path / rel
+        dst.parent.mkdir(parents=True, exist_ok=True)
+        shutil.copy(os.path.join(bench.ROOT, rel), dst)
+    monkeypatch.setattr(bench, "ROOT", str(tmp_path))
+    base = bench.kernel_source_digest()
+    k = tmp_path / bench.KERNEL_SOURCES[0]
+    src = k.read_text()
+    k.write_text("// a new comment line\n" + src.replace("namespace gms {", "namespace gms {  /* x */", 1))
+    assert bench.kernel_source_digest() == base
+    k.write_text(src.replace("constexpr int kWaves = 2;", "constexpr int kWaves = 4;", 1))
+    assert "constexpr int kWaves = 2;" in src and bench.kernel_source_digest() != base
+    k.write_text(src)
+    h = tmp_path / bench.HEADER
+    hs = h.read_text()
+    h.write_text(hs.replace("#define GMS_DEFAULT_CHUNK_BYTES (64u * 1024u)", "#define GMS_DEFAULT_CHUNK_BYTES (256u * 1024u)"))
+    assert bench.kernel_source_digest() != base
