@@ -151,8 +151,11 @@ int gms_layout(const gms_manifest *m, uint64_t *img_off, uint64_t *blk_base);
  * host image DMAs host slices into free slots on a library-owned copy stream
  * while the scatter kernel drains filled slots on the caller's stream; with
  * slots == 0 it reads the pinned image directly over the host link
- * (zero-copy) instead.  A snapshot into pinned host memory always writes it
- * zero-copy.  The image-file calls also use the ring (and a pinned host ring
+ * (zero-copy) instead.  A snapshot into pinned host memory runs the other
+ * way: the gather kernel fills a slot on the caller's stream and the copy
+ * stream DMAs it to the host image; with slots == 0, or slices below 128 MiB
+ * (where the device-to-host DMA loses half the link and more), it writes the
+ * image zero-copy.  The image-file calls also use the ring (and a pinned host ring
  * of twice the slots) and need slots > 0.  slice_bytes 0 selects
  * GMS_DEFAULT_SLICE_BYTES; a new manifest starts with GMS_DEFAULT_SLICE_BYTES x
  * GMS_DEFAULT_SLOTS (256 MiB slices keep the host link at about 99% of its

@@ -254,16 +254,26 @@ int run_direct(const gms_manifest *m, int op, uint8_t *image, const HashOut &h, 
     return e == hipSuccess ? GMS_OK : fail_hip(e, "kernel launch");
 }
 
-// Pinned image restored through the staging ring: DMA slice -> device slot on
-// the copy stream, scatter slot -> entries on the caller's stream, and the
-// copy stream refills a slot only after the kernel that read it.
-int run_ring(gms_manifest *m, const HashOut &h, uint8_t *host_image, hipStream_t s)
+// Slices below this size make a snapshot's device-to-host DMA erratic (half the
+// link and less with 64 MiB pieces); from 128 MiB up it holds about 99% of the
+// link, ahead of zero-copy stores (about 96%).
+constexpr uint64_t kRingSnapshotMinSlice = 128ull << 20;
+
+// A pinned image through the staging ring.  Restore: DMA slice -> device slot
+// on the copy stream, then the scatter kernel reads the slot on the caller's
+// stream.  Snapshot: the gather kernel fills the slot on the caller's stream,
+// then the copy stream DMAs it to the host image.  The slot's producer reuses
+// it only after its consumer is done with it.
+int run_ring(gms_manifest *m, int op, const HashOut &h, uint8_t *host_image, hipStream_t s)
 {
     int rc = ensure_ring(m);
     if (rc != GMS_OK) return rc;
     const uint64_t slice = m->ring_slice;
     const uint32_t k = m->ring_slots;
     const uint64_t nslices = ceil_div(m->image_bytes, slice);
+    const bool to_host = op == gms::kSnapshot;
+    hipStream_t producer = to_host ? s : m->copy_stream;
+    hipStream_t consumer = to_host ? m->copy_stream : s;
     hipError_t e;
 #define GMS_TRY(call)                                   \
     do {                                                \
@@ -283,23 +293,30 @@ int run_ring(gms_manifest *m, const HashOut &h, uint8_t *host_image, hipStream_t
         const uint64_t lo = sl * slice;
         const uint64_t bytes = std::min(slice, m->image_bytes - lo);
         const uint64_t c0 = m->slice_first[sl], c1 = m->slice_first[sl + 1];
-        if (sl >= k) GMS_TRY(hipStreamWaitEvent(m->copy_stream, m->ev_free[slot], 0));
-        GMS_TRY(hipMemcpyAsync(dev, host_image + lo, bytes, hipMemcpyHostToDevice, m->copy_stream));
-        GMS_TRY(hipEventRecord(m->ev_filled[slot], m->copy_stream));
-        GMS_TRY(hipStreamWaitEvent(s, m->ev_filled[slot], 0));
-        GMS_TRY(gms::launch_stream(gms::kRestore, h.any(), m->d_chunks, c0, c1 - c0, m->max_chunk, dev, lo, h, s));
-        GMS_TRY(hipEventRecord(m->ev_free[slot], s));
+        if (sl >= k) GMS_TRY(hipStreamWaitEvent(producer, m->ev_free[slot], 0));
+        if (to_host)
+            GMS_TRY(gms::launch_stream(op, h.any(), m->d_chunks, c0, c1 - c0, m->max_chunk, dev, lo, h, s));
+        else
+            GMS_TRY(hipMemcpyAsync(dev, host_image + lo, bytes, hipMemcpyHostToDevice, m->copy_stream));
+        GMS_TRY(hipEventRecord(m->ev_filled[slot], producer));
+        GMS_TRY(hipStreamWaitEvent(consumer, m->ev_filled[slot], 0));
+        if (to_host)
+            GMS_TRY(hipMemcpyAsync(host_image + lo, dev, bytes, hipMemcpyDeviceToHost, m->copy_stream));
+        else
+            GMS_TRY(gms::launch_stream(op, h.any(), m->d_chunks, c0, c1 - c0, m->max_chunk, dev, lo, h, s));
+        GMS_TRY(hipEventRecord(m->ev_free[slot], consumer));
     }
-    GMS_TRY(hipEventRecord(m->ev_done, s));
+    // the call ends on the caller's stream once the last slot is consumed
+    GMS_TRY(hipEventRecord(m->ev_done, consumer));
+    if (to_host) GMS_TRY(hipStreamWaitEvent(s, m->ev_done, 0));
     m->done_recorded = true;
 #undef GMS_TRY
     return GMS_OK;
 }
 
-// Device images take one launch.  A pinned image is written by a snapshot
-// with zero-copy stores straight over the host link (steadier and faster than
-// a device slot plus DMA) and read by a restore through the staging ring, or
-// zero-copy when the manifest has no ring slots.
+// Device images take one launch.  A pinned image goes through the staging
+// ring, except with no ring slots, and except a snapshot with slices below
+// kRingSnapshotMinSlice: those access the image zero-copy over the host link.
 int run_op(const gms_manifest *cm, int op, void *image, int kind, const HashOut &h, void *stream)
 {
     gms_manifest *m = const_cast<gms_manifest *>(cm);
@@ -311,7 +328,9 @@ int run_op(const gms_manifest *cm, int op, void *image, int kind, const HashOut 
     if (m->chunks.empty()) return GMS_OK;
     if (op == gms::kVerify || kind == GMS_MEM_DEVICE) return run_direct(m, op, (uint8_t *)image, h, s);
     std::lock_guard<std::mutex> lock(m->ring_mu);
-    if (op == gms::kSnapshot || m->slots == 0) {
+    const bool zero_copy =
+        m->slots == 0 || (op == gms::kSnapshot && gms::effective_slice(m) < kRingSnapshotMinSlice);
+    if (zero_copy) {
         void *dev = nullptr;
         e = hipHostGetDevicePointer(&dev, image, 0);
         if (e != hipSuccess) return fail_hip(e, "hipHostGetDevicePointer");
@@ -319,7 +338,7 @@ int run_op(const gms_manifest *cm, int op, void *image, int kind, const HashOut 
             return fail_hip(e, "ring order");
         return run_direct(m, op, (uint8_t *)dev, h, s);
     }
-    return run_ring(m, h, (uint8_t *)image, s);
+    return run_ring(m, op, h, (uint8_t *)image, s);
 }
 
 }  // namespace

@@ -209,6 +209,30 @@ def test_ragged_manifest_pinned(staging):
     assert all(np.array_equal(a, b) for a, b in zip(back, datas)) and arena.outside_untouched(whole)
 
 
+def test_pinned_snapshot_ring_across_slices():
+    """A 340 MiB ragged image through 128 MiB x 2 slots: three slices, the ring wraps and slice
+    edges fall inside entries.  Snapshot (gather kernel into a device slot, DMA to the host
+    image), restore and verify equal the oracle; with 64 MiB slices the snapshot writes
+    zero-copy instead and gives the same image and hashes."""
+    need_gpu()
+    sizes = [(100 << 20) + 7, 13, (150 << 20) + 3 * 4096 + 5, 0, (90 << 20) + 4095]
+    arena = Arena(sizes, misalign=lambda r: r.integers(0, 16), seed=21)
+    datas = random_datas(sizes, seed=21)
+    arena.fill(datas)
+    m, img = _round_trip(arena, datas, gms.MEM_HOST_PINNED, staging=(128 << 20, 2))
+    assert m.image_bytes > 2 * (128 << 20)
+    o_blk, o_ten = oracle.hashes(datas)
+    m.set_staging(64 << 20, 2)
+    img2 = _image(m.image_bytes, gms.MEM_HOST_PINNED)
+    blk, ten = u64_dev(m.num_blocks), u64_dev(m.num_entries)
+    gms.snapshot(m, img2, m.image_bytes, gms.MEM_HOST_PINNED, blk_hash=blk, ten_hash=ten)
+    torch.cuda.synchronize()
+    assert np.array_equal(img2.numpy()[: m.image_bytes], img.numpy()[: m.image_bytes])
+    assert np.array_equal(to_u64(blk, m.num_blocks), o_blk)
+    assert np.array_equal(to_u64(ten, m.num_entries), o_ten)
+    m.close()
+
+
 def test_plain_copy_without_hashes():
     need_gpu()
     sizes = [1 << 20, 4097, 123, 8 << 20]
