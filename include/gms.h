@@ -65,6 +65,11 @@
  *  - Calls on one manifest that use the pinned-host staging ring are ordered
  *    by the library; other calls that write the same memory from different
  *    streams race, as any two kernels would.
+ *  - Snapshot, restore and verify on device images only launch kernels on
+ *    `stream` (the zeroing of outputs included), so they can be captured into
+ *    a HIP graph and replayed; each replay recomputes every output.  Calls on
+ *    pinned-host images, the image-file calls and the store's verifications
+ *    return GMS_ERR_STATE while `stream` is capturing, and record nothing.
  *  - No exception, abort or hipMalloc failure crosses the ABI: each call
  *    returns a status; gms_last_error() gives the calling thread's last
  *    message.

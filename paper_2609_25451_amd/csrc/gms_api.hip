@@ -117,6 +117,15 @@ int ensure_ring(gms_manifest *m)
     return GMS_OK;
 }
 
+int refuse_capture(hipStream_t s, const char *what)
+{
+    hipStreamCaptureStatus cap = hipStreamCaptureStatusNone;
+    hipError_t e = hipStreamIsCapturing(s, &cap);
+    if (e != hipSuccess) return fail_hip(e, "hipStreamIsCapturing");
+    if (cap != hipStreamCaptureStatusNone) return fail(GMS_ERR_STATE, "%s: not allowed under stream capture", what);
+    return GMS_OK;
+}
+
 int ensure_host_ring(gms_manifest *m)
 {
     int rc = ensure_ring(m);
@@ -323,10 +332,16 @@ int run_op(const gms_manifest *cm, int op, void *image, int kind, const HashOut 
     DeviceGuard g(m->device);
     if (g.err != hipSuccess) return fail_hip(g.err, "hipSetDevice");
     hipStream_t s = (hipStream_t)stream;
-    hipError_t e = gms::launch_prologue(h, m->n, s);
-    if (e != hipSuccess) return fail_hip(e, "prologue launch");
+    hipError_t e;
+    const bool pinned = op != gms::kVerify && kind != GMS_MEM_DEVICE;
+    // the pinned-host paths order themselves across calls with events on the
+    // library's copy stream, which a captured graph could not replay faithfully
+    int rc;
+    if (pinned && (rc = gms::refuse_capture(s, "a pinned-host image (device images can be captured)")) != GMS_OK)
+        return rc;
+    if ((e = gms::launch_prologue(h, m->n, s)) != hipSuccess) return fail_hip(e, "prologue launch");
     if (m->chunks.empty()) return GMS_OK;
-    if (op == gms::kVerify || kind == GMS_MEM_DEVICE) return run_direct(m, op, (uint8_t *)image, h, s);
+    if (!pinned) return run_direct(m, op, (uint8_t *)image, h, s);
     std::lock_guard<std::mutex> lock(m->ring_mu);
     const bool zero_copy =
         m->slots == 0 || (op == gms::kSnapshot && gms::effective_slice(m) < kRingSnapshotMinSlice);

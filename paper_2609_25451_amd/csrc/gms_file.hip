@@ -298,6 +298,7 @@ int gms_restore_from_file(const gms_manifest *cm, const char *path, uint64_t fil
     DeviceGuard g(m->device);
     if (g.err != hipSuccess) return fail_hip(g.err, "hipSetDevice");
     hipStream_t s = (hipStream_t)stream;
+    if ((rc = gms::refuse_capture(s, "an image-file call")) != GMS_OK) return rc;
     GMS_TRY(gms::launch_prologue(h, m->n, s));
     if (m->chunks.empty()) return GMS_OK;
 
@@ -358,6 +359,7 @@ int gms_snapshot_to_file(const gms_manifest *cm, const char *path, uint32_t flag
     DeviceGuard g(m->device);
     if (g.err != hipSuccess) return fail_hip(g.err, "hipSetDevice");
     hipStream_t s = (hipStream_t)stream;
+    if ((rc = gms::refuse_capture(s, "an image-file call")) != GMS_OK) return rc;
     GMS_TRY(gms::launch_prologue(h, m->n, s));
     if (m->chunks.empty()) {
         GMS_TRY(hipStreamSynchronize(s));

@@ -87,6 +87,9 @@ int ensure_ring(gms_manifest *m);       // device slots, copy stream, events, sl
 int ensure_host_ring(gms_manifest *m);  // plus pinned host slots
 int check_common(const gms_manifest *m, const void *image, uint64_t image_bytes, int kind, bool need_image);
 int check_outputs(const gms_manifest *m, const HashOut &h);
+// GMS_ERR_STATE if `s` is capturing a graph: for calls that synchronize or
+// order themselves with library-owned streams and events.
+int refuse_capture(hipStream_t s, const char *what);
 HashOut make_hash(const uint64_t *expected, uint64_t *blk, uint64_t *ten, uint64_t *cnt, uint64_t *list,
                   uint64_t cap);
 

@@ -56,8 +56,10 @@ int hash_and_compare(gms_store *s, const gms_manifest *m, const uint64_t *expect
                      uint64_t *list, uint64_t cap, uint64_t *count, void *stream)
 {
     *count = 0;
+    int rc = gms::refuse_capture((hipStream_t)stream, "a store verification");
+    if (rc != GMS_OK) return rc;
     if (gms_num_blocks(m) == 0) return GMS_OK;
-    int rc = gms_verify(m, expected, hash_out, nullptr, expected ? s->d_count : nullptr, expected ? list : nullptr,
+    rc = gms_verify(m, expected, hash_out, nullptr, expected ? s->d_count : nullptr, expected ? list : nullptr,
                         expected ? cap : 0, stream);
     if (rc != GMS_OK) return rc;
     hipStream_t st = (hipStream_t)stream;

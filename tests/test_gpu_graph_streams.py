@@ -1,9 +1,12 @@
 """Capture in a HIP graph and concurrent streams.
 
-A device-image restore launches only kernels (the prologue that zeroes the
-counters is a kernel, not a memset), so it can be captured once and replayed;
-every replay is checked against the oracle with eager work in between.
-Independent manifests restored on two streams at once must not interfere.
+A device-image restore, snapshot or verify launches only kernels (the prologue
+that zeroes the counters is a kernel, not a memset), so it can be captured
+once and replayed; every replay is checked against the oracle for the bytes
+the memory holds at that moment, with eager work in between.  Calls that
+cannot be captured (pinned-host images, image files, store verification)
+refuse with GMS_ERR_STATE and leave the capture usable.  Independent
+manifests restored on two streams at once must not interfere.
 """
 import numpy as np
 import pytest
@@ -14,6 +17,15 @@ import paper_2609_25451_amd as gms
 from gpu_util import Arena, from_u64, need_gpu, random_datas, to_u64, u64_dev
 
 pytestmark = pytest.mark.gpu
+
+SIZES = [70_000, 13, 0, 3 * 4096, (2 << 20) + 5, 4095, 200_001]
+
+
+def _arena(seed):
+    arena = Arena(SIZES, misalign=lambda r: r.integers(0, 16), seed=seed)
+    datas = random_datas(SIZES, seed=seed)
+    arena.fill(datas)
+    return arena, datas
 
 
 def _setup(seed, sizes):
@@ -90,3 +102,99 @@ def test_independent_manifests_on_two_streams():
             assert to_u64(cnt)[0] == 0
             assert np.array_equal(to_u64(blk, m.num_blocks), o_blk)
             assert np.array_equal(to_u64(ten, m.num_entries), o_ten)
+
+
+def test_captured_snapshot_and_verify_follow_the_data():
+    """One graph holds a snapshot (image, block and tensor hashes) and a verify against an
+    earlier hash array; the entries change eagerly between replays."""
+    need_gpu()
+    arena, datas = _arena(62)
+    m = gms.Manifest(arena.entries)
+    o_blk0, _ = oracle.hashes(datas)
+    exp = from_u64(o_blk0)
+    img = torch.empty(m.image_bytes, dtype=torch.uint8, device="cuda")
+    blk, ten, vcnt = u64_dev(m.num_blocks), u64_dev(m.num_entries), u64_dev(1)
+
+    def step():
+        gms.snapshot(m, img, m.image_bytes, blk_hash=blk, ten_hash=ten)
+        gms.verify(m, expected=exp, mismatch_count=vcnt)
+
+    step()  # warm the kernels outside capture
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        step()
+    torch.cuda.synchronize()
+
+    rng = np.random.default_rng(5)
+    cur = [d.copy() for d in datas]
+    for rep in range(4):
+        if rep:  # rewrite a few bytes of random non-empty entries
+            for _ in range(rep):
+                i = int(rng.choice([k for k, n in enumerate(SIZES) if n]))
+                j = int(rng.integers(0, SIZES[i]))
+                cur[i][j] ^= 0xFF
+                arena.view(i)[j] = int(cur[i][j])
+        img.fill_(0xEE)
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        o_blk, o_ten = oracle.hashes(cur)
+        assert np.array_equal(img.cpu().numpy(), oracle.pack(cur)), f"replay {rep}: image"
+        assert np.array_equal(to_u64(blk, m.num_blocks), o_blk), f"replay {rep}: block hashes"
+        assert np.array_equal(to_u64(ten, m.num_entries), o_ten), f"replay {rep}: tensor hashes"
+        assert to_u64(vcnt)[0] == oracle.verify(cur, o_blk0)[0], f"replay {rep}: verify count"
+    del g
+    m.close()
+
+
+def test_uncapturable_calls_refuse_and_leave_the_capture_usable(tmp_path):
+    need_gpu()
+    arena, datas = _arena(63)
+    m = gms.Manifest(arena.entries)
+    o_img = oracle.pack(datas)
+    pinned = torch.from_numpy(o_img.copy()).pin_memory()
+    path = tmp_path / "image.bin"
+    o_img.tofile(path)
+    dev_img = torch.from_numpy(o_img).cuda()
+    s = gms.Store(va_bytes=1 << 30, slab_bytes=8 << 20)
+    with s.connect_rw() as w:
+        a = w.alloc(4096)
+        w.commit([(a, 4096)])
+    reader = s.connect_ro()
+
+    refused = []
+    gms.restore(m, dev_img, m.image_bytes)  # warm the kernels outside capture
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        for name, call in (
+            ("pinned restore", lambda: gms.restore(m, pinned, m.image_bytes, gms.MEM_HOST_PINNED)),
+            ("pinned snapshot", lambda: gms.snapshot(m, pinned, m.image_bytes, gms.MEM_HOST_PINNED)),
+            ("file restore", lambda: gms.restore_from_file(m, path, flags=0)),
+            ("store verify", lambda: s.verify()),
+        ):
+            try:
+                call()
+            except gms.GmsError as e:
+                refused.append((name, e.status))
+        gms.restore(m, dev_img, m.image_bytes)
+    torch.cuda.synchronize()
+    assert refused == [(n, gms.GMS_ERR_STATE) for n in
+                       ("pinned restore", "pinned snapshot", "file restore", "store verify")]
+    arena.poison()
+    torch.cuda.synchronize()
+    g.replay()
+    torch.cuda.synchronize()
+    back, whole = arena.read()
+    assert all(np.array_equal(a, b) for a, b in zip(back, datas)) and arena.outside_untouched(whole)
+    # the same calls work again outside capture
+    arena.poison()
+    gms.restore(m, pinned, m.image_bytes, gms.MEM_HOST_PINNED)
+    torch.cuda.synchronize()
+    assert all(np.array_equal(a, b) for a, b in zip(arena.read()[0], datas))
+    assert s.verify() == 0
+    reader.close()
+    del g
+    m.close()
+    s.close()
