@@ -57,7 +57,8 @@
  *    falls outside one.  The image base must be 16-byte aligned.
  *  - Hash/mismatch arrays are uint64_t device arrays: blk_hash has
  *    gms_num_blocks() entries, ten_hash gms_num_entries(), mismatch_count one,
- *    mismatch_list `mismatch_cap`.  Every output pointer may be NULL unless
+ *    mismatch_list min(mismatch_cap, gms_num_blocks()) (a call records each
+ *    block at most once).  Every output pointer may be NULL unless
  *    stated otherwise; with all of them NULL the call is a plain copy.
  *  - A verify mismatch is not an error: the call returns GMS_OK and the count
  *    is > 0.  The mismatch list holds min(count, cap) global block indices in
@@ -161,8 +162,8 @@ int gms_layout(const gms_manifest *m, uint64_t *img_off, uint64_t *blk_base);
  * stream DMAs it to the host image; with slots == 0, or slices below 128 MiB
  * (where the device-to-host DMA loses half the link and more), it writes the
  * image zero-copy.  The image-file calls also use the ring (and a pinned host ring
- * of twice the slots) and need slots > 0.  slice_bytes 0 selects
- * GMS_DEFAULT_SLICE_BYTES; a new manifest starts with GMS_DEFAULT_SLICE_BYTES x
+ * of twice the slots) and need slots > 0.  slice_bytes is 0, which selects
+ * GMS_DEFAULT_SLICE_BYTES, or in [4096, 64 GiB]; slots at most 16; a new manifest starts with GMS_DEFAULT_SLICE_BYTES x
  * GMS_DEFAULT_SLOTS (256 MiB slices keep the host link at about 99% of its
  * peak; 64 MiB slices reach about 97.5%).  Takes effect at the next ring
  * call; frees the old rings after draining them.  Synchronous.
@@ -228,7 +229,8 @@ enum gms_file_flags {
  * and enqueued; device work completes on `stream`.  The first file call
  * allocates the manifest's pinned host ring: 2 x slots (at most 16) slices.
  * Errors: as gms_restore, plus GMS_ERR_IO (open/read failure) and
- * GMS_ERR_SIZE (file shorter than file_offset + gms_image_bytes).  After an
+ * GMS_ERR_SIZE (file shorter than file_offset + gms_image_bytes), and
+ * GMS_ERR_INVALID for a file_offset no file can reach.  After an
  * I/O error, slices already read may have been restored (and counted in the
  * hash outputs): the entries and outputs are then partial and must not be
  * used; the manifest stays usable.
@@ -278,7 +280,8 @@ void gms_pool_destroy(gms_pool *p);
 
 /* First fit in mapped slabs (a new slab is mapped when none fits); an allocation larger
  * than a slab gets a dedicated mapping.  align: power of two <= granularity, 0 = 256.
- * Errors: GMS_ERR_INVALID, GMS_ERR_NOMEM (reservation or device memory exhausted). */
+ * Errors: GMS_ERR_INVALID, GMS_ERR_NOMEM (reservation or device memory exhausted, or
+ * bytes above the pool's VA budget). */
 int gms_pool_alloc(gms_pool *p, uint64_t bytes, uint64_t align, uint64_t *addr_out);
 
 /* Returns an allocation; a dedicated mapping is unmapped and released, with its VA.

@@ -22,6 +22,7 @@ using gms::fail_hip;
 using gms::kMaxChunk;
 using gms::kDefaultSlice;
 using gms::kMaxSlots;
+using gms::kMaxSlice;
 
 namespace {
 thread_local std::string g_last_error;
@@ -227,8 +228,10 @@ int check_outputs(const gms_manifest *m, const HashOut &h)
         if ((rc = check_device_range(h.expected, m->num_blocks * 8, m->device, "expected_blk")) != GMS_OK) return rc;
         if (!h.mm_count) return fail(GMS_ERR_INVALID, "expected_blk given without mismatch_count_out");
         if ((rc = check_device_range(h.mm_count, 8, m->device, "mismatch_count")) != GMS_OK) return rc;
-        if (h.mm_list && h.mm_cap &&
-            (rc = check_device_range(h.mm_list, h.mm_cap * 8, m->device, "mismatch_list")) != GMS_OK)
+        // a call records each block at most once, so at most min(cap, blocks) list entries are written
+        const uint64_t written = std::min<uint64_t>(h.mm_cap, m->num_blocks);
+        if (h.mm_list && written &&
+            (rc = check_device_range(h.mm_list, written * 8, m->device, "mismatch_list")) != GMS_OK)
             return rc;
     }
     return GMS_OK;
@@ -535,7 +538,8 @@ int gms_manifest_set_staging(gms_manifest *m, uint64_t slice_bytes, uint32_t slo
     if (!m) return fail(GMS_ERR_INVALID, "manifest is null");
     if (m->device < 0) return fail(GMS_ERR_STATE, "host-only manifest has no device");
     if (slots > kMaxSlots) return fail(GMS_ERR_INVALID, "slots %u > %u", slots, kMaxSlots);
-    if (slots && slice_bytes < GMS_BLOCK_BYTES) return fail(GMS_ERR_INVALID, "slice_bytes %llu", (unsigned long long)slice_bytes);
+    if (slice_bytes && (slice_bytes < GMS_BLOCK_BYTES || slice_bytes > kMaxSlice))
+        return fail(GMS_ERR_INVALID, "slice_bytes %llu is outside [4096, 64 GiB]", (unsigned long long)slice_bytes);
     std::lock_guard<std::mutex> lock(m->ring_mu);
     DeviceGuard g(m->device);
     free_ring(m);

@@ -22,6 +22,7 @@
 #include <algorithm>
 #include <atomic>
 #include <cerrno>
+#include <cstdint>
 #include <condition_variable>
 #include <cstdlib>
 #include <cstring>
@@ -287,6 +288,8 @@ int gms_restore_from_file(const gms_manifest *cm, const char *path, uint64_t fil
     gms_manifest *m = const_cast<gms_manifest *>(cm);
     const unsigned threads = io_threads ? io_threads : kDefaultIoThreads;
 
+    if (file_offset > (uint64_t)INT64_MAX - m->image_bytes)
+        return fail(GMS_ERR_INVALID, "file_offset %llu is past any file position", (unsigned long long)file_offset);
     FileHandle f;
     if ((rc = open_file(f, path, false, flags & GMS_FILE_DIRECT, file_offset)) != GMS_OK) return rc;
     struct stat st;

@@ -17,6 +17,7 @@ constexpr uint64_t kMaxChunk = 64ull << 20;
 constexpr uint64_t kDefaultSlice = GMS_DEFAULT_SLICE_BYTES;
 constexpr uint32_t kDefaultSlots = GMS_DEFAULT_SLOTS;
 constexpr uint32_t kMaxSlots = 16;
+constexpr uint64_t kMaxSlice = 64ull << 30;
 
 inline uint64_t ceil_div(uint64_t a, uint64_t b) { return a / b + (a % b != 0); }
 

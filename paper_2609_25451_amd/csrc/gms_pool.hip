@@ -308,6 +308,9 @@ int gms_pool_alloc(gms_pool *p, uint64_t bytes, uint64_t align, uint64_t *addr_o
     if (bytes == 0 || (align & (align - 1)) || align > p->gran)
         return fail(GMS_ERR_INVALID, "bytes %llu / align %llu (power of two <= %llu)", (unsigned long long)bytes,
                     (unsigned long long)align, (unsigned long long)p->gran);
+    if (bytes > p->reserved)
+        return fail(GMS_ERR_NOMEM, "%llu bytes exceed the pool's VA budget of %llu", (unsigned long long)bytes,
+                    (unsigned long long)p->reserved);
     std::lock_guard<std::mutex> lock(p->mu);
     DeviceGuard g(p->device);
     if (g.err != hipSuccess) return fail_hip(g.err, "hipSetDevice");

@@ -60,7 +60,7 @@ int hash_and_compare(gms_store *s, const gms_manifest *m, const uint64_t *expect
     if (rc != GMS_OK) return rc;
     if (gms_num_blocks(m) == 0) return GMS_OK;
     rc = gms_verify(m, expected, hash_out, nullptr, expected ? s->d_count : nullptr, expected ? list : nullptr,
-                        expected ? cap : 0, stream);
+                    expected ? cap : 0, stream);
     if (rc != GMS_OK) return rc;
     hipStream_t st = (hipStream_t)stream;
     hipError_t e;

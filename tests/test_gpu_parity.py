@@ -363,3 +363,54 @@ def test_argument_errors_on_gpu():
     with pytest.raises(gms.GmsError) as e:
         gms.verify(m)
     assert e.value.status == gms.GMS_ERR_INVALID
+
+
+def test_sizes_that_would_wrap_are_refused():
+    """Byte counts that would overflow 64 bits are refused before anything is enqueued."""
+    need_gpu()
+    hip = ctypes.CDLL("libamdhip64.so.7")
+    ent = torch.zeros(1 << 30, dtype=torch.uint8, device="cuda")
+    m = gms.Manifest([(ent.data_ptr(), 1 << 30)], device=0)  # 2^18 blocks
+    exp, cnt = u64_dev(m.num_blocks), u64_dev(1)
+    gms.verify(m, blk_hash=exp)
+    lists = []
+    for nbytes in (1 << 20, 2 << 20):  # exact allocations: 2^17 and 2^18 list entries
+        raw = ctypes.c_void_p()
+        assert hip.hipMalloc(ctypes.byref(raw), ctypes.c_size_t(nbytes)) == 0
+        lists.append(raw.value)
+    try:
+        # a capacity whose byte count wraps to 8: the list holds half the entries one call can write
+        with pytest.raises(gms.GmsError) as e:
+            gms.verify(m, expected=exp, mismatch_count=cnt, mismatch_list=lists[0], mismatch_cap=(1 << 61) + 1)
+        assert e.value.status == gms.GMS_ERR_SIZE
+        # a list as long as the block count takes any capacity
+        gms.verify(m, expected=exp, mismatch_count=cnt, mismatch_list=lists[1], mismatch_cap=(1 << 64) - 1)
+        torch.cuda.synchronize()
+        assert to_u64(cnt)[0] == 0
+    finally:
+        for a in lists:
+            hip.hipFree(ctypes.c_void_p(a))
+    for slice_bytes, slots in ((100, 1), (128 << 30, 1), (1 << 63, 2), (4096, 17)):
+        with pytest.raises(gms.GmsError) as e:
+            m.set_staging(slice_bytes, slots)
+        assert e.value.status == gms.GMS_ERR_INVALID, (slice_bytes, slots)
+    with pytest.raises(gms.GmsError) as e:
+        gms.restore_from_file(m, "/nonexistent/image", file_offset=(1 << 64) - 4096)
+    assert e.value.status == gms.GMS_ERR_INVALID
+    m.close()
+    del ent
+    pool = gms.Pool(va_bytes=1 << 30, slab_bytes=8 << 20)
+    for nbytes in ((1 << 64) - 1, (1 << 30) + 1):
+        with pytest.raises(gms.GmsError) as e:
+            pool.alloc(nbytes)
+        assert e.value.status == gms.GMS_ERR_NOMEM, nbytes
+    pool.close()
+
+
+def test_staging_slice_zero_selects_the_default():
+    need_gpu()
+    sizes = [300_000, 5, 4096 * 3]
+    arena = Arena(sizes, seed=4)
+    datas = random_datas(sizes, seed=4)
+    arena.fill(datas)
+    _round_trip(arena, datas, gms.MEM_HOST_PINNED, staging=(0, 3))
