@@ -124,11 +124,19 @@ def _check(rc: int, call: str) -> None:
         raise GmsError(rc, call)
 
 
+def _dense(t):
+    """A tensor stands for the bytes [data_ptr, data_ptr + numel * element_size): only a
+    contiguous one does."""
+    if hasattr(t, "is_contiguous") and not t.is_contiguous():
+        raise ValueError("a non-contiguous tensor does not describe one byte range; pass .contiguous()")
+    return t
+
+
 def _ptr(x) -> int | None:
     if x is None:
         return None
     if hasattr(x, "data_ptr"):
-        return int(x.data_ptr())
+        return int(_dense(x).data_ptr())
     return int(x)
 
 
@@ -155,7 +163,7 @@ def _ranges(entries):
     out = []
     for e in entries:
         if hasattr(e, "data_ptr"):
-            out.append((int(e.data_ptr()), int(e.numel() * e.element_size())))
+            out.append((int(_dense(e).data_ptr()), int(e.numel() * e.element_size())))
         else:
             out.append((int(e[0]), int(e[1])))
     return out

@@ -134,3 +134,22 @@ def test_null_arguments():
     assert gms.gms_restore_from_file(m.handle, None, 0, 0, 0, None, None, None, None, None, 0, None) == gms.GMS_ERR_STATE
     for rc in (0, -1, -2, -3, -4, -5, -6, -7, 7):
         assert gms.status_str(rc)
+
+
+def test_non_contiguous_tensors_refused_by_the_binding():
+    """A strided view is not the byte range [data_ptr, data_ptr + nbytes): the binding refuses it
+    as an entry, an image or an output array before any library call."""
+    import torch
+
+    t = torch.zeros(64, 64, dtype=torch.bfloat16)
+    col = t[:, 3]
+    assert not col.is_contiguous()
+    with pytest.raises(ValueError, match="non-contiguous"):
+        gms.Manifest([col], device=gms.HOST_ONLY)
+    m = gms.Manifest([t], device=gms.HOST_ONLY)
+    assert m.payload_bytes == t.numel() * 2
+    with pytest.raises(ValueError, match="non-contiguous"):
+        gms.snapshot(m, torch.zeros(4, 8192, dtype=torch.uint8)[:, ::2], m.image_bytes, stream=0)
+    with pytest.raises(ValueError, match="non-contiguous"):
+        gms.verify(m, blk_hash=torch.zeros(8, 2, dtype=torch.int64)[:, 0], stream=0)
+    m.close()
