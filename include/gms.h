@@ -242,13 +242,44 @@ int gms_restore_from_file(const gms_manifest *m, const char *path, uint64_t file
 
 /*
  * Writes the packed image to `path` (created or truncated): the kernel gathers
- * each slice into a slot of the pinned host ring and `io_threads` workers
+ * each slice into a slot of the pinned host ring (through a device slot and a
+ * DMA when slices are 128 MiB or more) and `io_threads` workers
  * (0 = 16) write its 16 MiB pieces with pwrite; optionally emits the
  * block / tensor hashes of the gathered bytes.  Synchronous: the file is
  * complete when the call returns (durable too with GMS_FILE_SYNC).
  * Errors: GMS_ERR_STATE, GMS_ERR_INVALID, GMS_ERR_IO, GMS_ERR_HIP, GMS_ERR_NOMEM.
  */
 int gms_snapshot_to_file(const gms_manifest *m, const char *path, uint32_t flags, uint32_t io_threads,
+                         uint64_t *blk_hash_out, uint64_t *ten_hash_out, void *stream);
+
+/*
+ * The packed image in ordinary host memory (pageable, or any host memory the
+ * calling process can read and write).  A process snapshot stages device
+ * state in the host memory of the checkpointed process and reinstates it on
+ * restore (paper section 3.1); the paper's checkpoint tool copies it back
+ * serially without saturating PCIe (section 5.2).  Here `threads` workers
+ * (0 = 16) copy 16 MiB pieces between `image` and the slots of the pinned host
+ * ring, and each slice goes through a device slot and the kernel as in
+ * gms_restore_from_file; no part of `image` has to be pinned.
+ *
+ * gms_restore_from_host returns when every slice has been copied out of
+ * `image` and enqueued (the caller may then reuse `image`); device work and
+ * the hash / mismatch outputs complete on `stream`, as gms_restore.
+ * gms_snapshot_to_host is synchronous: `image` holds the packed image (zero
+ * padding included) when it returns, and the optional hashes are complete.
+ * `image` is host memory of at least gms_image_bytes(m) bytes (NULL allowed
+ * for an empty layout); the library cannot check pageable memory beyond
+ * that, so a shorter or unmapped buffer is undefined behaviour.  Device
+ * memory is refused (GMS_ERR_INVALID: use gms_restore / gms_snapshot).
+ * Errors: GMS_ERR_STATE (host-only manifest, or `stream` capturing a graph),
+ * GMS_ERR_INVALID, GMS_ERR_SIZE (image_bytes below the layout), GMS_ERR_HIP,
+ * GMS_ERR_NOMEM (staging rings).
+ */
+int gms_restore_from_host(const gms_manifest *m, const void *image, uint64_t image_bytes, uint32_t threads,
+                          const uint64_t *expected_blk, uint64_t *blk_hash_out, uint64_t *ten_hash_out,
+                          uint64_t *mismatch_count_out, uint64_t *mismatch_list_out, uint64_t mismatch_cap,
+                          void *stream);
+int gms_snapshot_to_host(const gms_manifest *m, void *image, uint64_t image_bytes, uint32_t threads,
                          uint64_t *blk_hash_out, uint64_t *ten_hash_out, void *stream);
 
 /*
@@ -430,7 +461,8 @@ const char *gms_status_str(int status);
 /* The calling thread's last error message ("" if none); valid until its next call. */
 const char *gms_last_error(void);
 
-/* ABI version of this header (2: adds the model-state store and GMS_ERR_INTEGRITY). */
+/* ABI version of this header (2: adds the model-state store and GMS_ERR_INTEGRITY;
+ * 3: adds gms_restore_from_host and gms_snapshot_to_host). */
 int gms_abi_version(void);
 
 #ifdef __cplusplus

@@ -83,6 +83,8 @@ _verify = _sig("gms_verify", INT, [VP, VP, VP, VP, VP, VP, U64, VP])
 _restore_file = _sig("gms_restore_from_file", INT,
                      [VP, ctypes.c_char_p, U64, ctypes.c_uint32, ctypes.c_uint32, VP, VP, VP, VP, VP, U64, VP])
 _snapshot_file = _sig("gms_snapshot_to_file", INT, [VP, ctypes.c_char_p, ctypes.c_uint32, ctypes.c_uint32, VP, VP, VP])
+_restore_host = _sig("gms_restore_from_host", INT, [VP, VP, U64, ctypes.c_uint32, VP, VP, VP, VP, VP, U64, VP])
+_snapshot_host = _sig("gms_snapshot_to_host", INT, [VP, VP, U64, ctypes.c_uint32, VP, VP, VP])
 _pool_create = _sig("gms_pool_create", INT, [INT, U64, U64, ctypes.POINTER(VP)])
 _pool_destroy = _sig("gms_pool_destroy", None, [VP])
 _pool_alloc = _sig("gms_pool_alloc", INT, [VP, U64, U64, ctypes.POINTER(U64)])
@@ -137,7 +139,21 @@ def _ptr(x) -> int | None:
         return None
     if hasattr(x, "data_ptr"):
         return int(_dense(x).data_ptr())
+    if hasattr(x, "__array_interface__"):  # numpy arrays
+        if not x.flags["C_CONTIGUOUS"]:
+            raise ValueError("a non-contiguous array does not describe one byte range; pass a contiguous copy")
+        return int(x.ctypes.data)
     return int(x)
+
+
+def _nbytes(x, nbytes):
+    if nbytes is not None:
+        return int(nbytes)
+    if hasattr(x, "nbytes"):
+        return int(x.nbytes)
+    if hasattr(x, "numel"):
+        return int(x.numel() * x.element_size())
+    raise ValueError("image_bytes is needed for a raw pointer")
 
 
 def _stream(stream) -> int | None:
@@ -283,6 +299,23 @@ def snapshot_to_file(m: Manifest, path, flags: int = 0, io_threads: int = 0, blk
                      stream=None) -> None:
     _check(_snapshot_file(m._h, os.fsencode(path), flags, io_threads, _ptr(blk_hash), _ptr(ten_hash),
                           _stream(stream)), "gms_snapshot_to_file")
+
+
+def restore_from_host(m: Manifest, image, image_bytes: int | None = None, threads: int = 0, expected=None,
+                      blk_hash=None, ten_hash=None, mismatch_count=None, mismatch_list=None, mismatch_cap: int = 0,
+                      stream=None) -> None:
+    """Restore from an image in ordinary host memory (a numpy array, a CPU tensor or an
+    address): returns once `image` may be reused; device work completes on `stream`."""
+    _check(_restore_host(m._h, _ptr(image), _nbytes(image, image_bytes), threads, _ptr(expected), _ptr(blk_hash),
+                         _ptr(ten_hash), _ptr(mismatch_count), _ptr(mismatch_list), mismatch_cap, _stream(stream)),
+           "gms_restore_from_host")
+
+
+def snapshot_to_host(m: Manifest, image, image_bytes: int | None = None, threads: int = 0, blk_hash=None,
+                     ten_hash=None, stream=None) -> None:
+    """Snapshot into ordinary host memory; synchronous."""
+    _check(_snapshot_host(m._h, _ptr(image), _nbytes(image, image_bytes), threads, _ptr(blk_hash), _ptr(ten_hash),
+                          _stream(stream)), "gms_snapshot_to_host")
 
 
 class Pool:
@@ -477,6 +510,8 @@ gms_restore_from_file = _restore_file
 gms_pool_create = _pool_create
 gms_pool_alloc = _pool_alloc
 gms_snapshot_to_file = _snapshot_file
+gms_restore_from_host = _restore_host
+gms_snapshot_to_host = _snapshot_host
 gms_manifest_set_staging = _set_staging
 gms_status_str = _status_str
 gms_last_error = _last_error

@@ -266,11 +266,6 @@ int run_direct(const gms_manifest *m, int op, uint8_t *image, const HashOut &h, 
     return e == hipSuccess ? GMS_OK : fail_hip(e, "kernel launch");
 }
 
-// Slices below this size make a snapshot's device-to-host DMA erratic (half the
-// link and less with 64 MiB pieces); from 128 MiB up it holds about 99% of the
-// link, ahead of zero-copy stores (about 96%).
-constexpr uint64_t kRingSnapshotMinSlice = 128ull << 20;
-
 // A pinned image through the staging ring.  Restore: DMA slice -> device slot
 // on the copy stream, then the scatter kernel reads the slot on the caller's
 // stream.  Snapshot: the gather kernel fills the slot on the caller's stream,
@@ -328,7 +323,7 @@ int run_ring(gms_manifest *m, int op, const HashOut &h, uint8_t *host_image, hip
 
 // Device images take one launch.  A pinned image goes through the staging
 // ring, except with no ring slots, and except a snapshot with slices below
-// kRingSnapshotMinSlice: those access the image zero-copy over the host link.
+// gms::kRingSnapshotMinSlice: those access the image zero-copy over the host link.
 int run_op(const gms_manifest *cm, int op, void *image, int kind, const HashOut &h, void *stream)
 {
     gms_manifest *m = const_cast<gms_manifest *>(cm);
@@ -347,7 +342,7 @@ int run_op(const gms_manifest *cm, int op, void *image, int kind, const HashOut 
     if (!pinned) return run_direct(m, op, (uint8_t *)image, h, s);
     std::lock_guard<std::mutex> lock(m->ring_mu);
     const bool zero_copy =
-        m->slots == 0 || (op == gms::kSnapshot && gms::effective_slice(m) < kRingSnapshotMinSlice);
+        m->slots == 0 || (op == gms::kSnapshot && gms::effective_slice(m) < gms::kRingSnapshotMinSlice);
     if (zero_copy) {
         void *dev = nullptr;
         e = hipHostGetDevicePointer(&dev, image, 0);
@@ -369,7 +364,7 @@ using gms::make_hash;
 
 extern "C" {
 
-int gms_abi_version(void) { return 2; }
+int gms_abi_version(void) { return 3; }
 
 const char *gms_status_str(int status)
 {

@@ -1,0 +1,179 @@
+"""Images in ordinary (pageable) host memory against the oracle.
+
+gms_snapshot_to_host gathers through the staging rings into a numpy buffer the
+library never pins; gms_restore_from_host copies a numpy image through the
+same rings into the entries.  Images, hashes, restored bytes (and the bytes
+around them) and mismatch lists are compared with the oracle over ring
+geometries that take both snapshot routes (device slot + DMA for slices of
+128 MiB and more, zero-copy into the host slot below), several worker counts,
+ring wrap-around and slice edges inside entries.
+"""
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2609_25451_amd as gms
+from gpu_util import Arena, from_u64, need_gpu, random_datas, to_u64, u64_dev
+
+pytestmark = pytest.mark.gpu
+
+RAGGED = [300_001, 13, 0, 4096 * 7, (3 << 20) + 5, 4095, 1 << 20, 77_777]
+
+
+def _setup(sizes, seed, misalign=True):
+    arena = Arena(sizes, misalign=(lambda r: r.integers(0, 16)) if misalign else None, seed=seed)
+    datas = random_datas(sizes, seed=seed)
+    arena.fill(datas)
+    return arena, datas
+
+
+def _host_round_trip(arena, datas, staging=None, threads=0):
+    m = gms.Manifest(arena.entries)
+    if staging is not None:
+        m.set_staging(*staging)
+    o_img = oracle.pack(datas)
+    o_blk, o_ten = oracle.hashes(datas)
+    nb, n = m.num_blocks, m.num_entries
+
+    img = np.full(m.image_bytes, 0x5A, dtype=np.uint8)
+    blk, ten = u64_dev(nb), u64_dev(n)
+    gms.snapshot_to_host(m, img, threads=threads, blk_hash=blk, ten_hash=ten)
+    assert np.array_equal(img, o_img), "host snapshot differs from the oracle image"
+    torch.cuda.synchronize()
+    assert np.array_equal(to_u64(blk, nb), o_blk) and np.array_equal(to_u64(ten, n), o_ten)
+
+    arena.poison()
+    src = o_img.copy()
+    cnt, lst, blk2, ten2 = u64_dev(1), u64_dev(8), u64_dev(nb), u64_dev(n)
+    gms.restore_from_host(m, src, threads=threads, expected=from_u64(o_blk), blk_hash=blk2, ten_hash=ten2,
+                          mismatch_count=cnt, mismatch_list=lst, mismatch_cap=8)
+    torch.cuda.synchronize()
+    back, whole = arena.read()
+    assert all(np.array_equal(a, b) for a, b in zip(back, datas)), "restored entries differ"
+    assert arena.outside_untouched(whole), "restore wrote outside the manifest"
+    assert to_u64(cnt)[0] == 0
+    assert np.array_equal(to_u64(blk2, nb), o_blk) and np.array_equal(to_u64(ten2, n), o_ten)
+    return m, o_img, o_blk
+
+
+@pytest.mark.parametrize("staging,threads", [(None, 0), ((1 << 20, 3), 3), ((64 << 10, 1), 1), ((4 << 20, 16), 64)],
+                         ids=["default", "1m_x3_t3", "64k_x1_t1", "4m_x16_t64"])
+def test_host_round_trip(staging, threads):
+    need_gpu()
+    arena, datas = _setup(RAGGED, seed=51)
+    m, _, _ = _host_round_trip(arena, datas, staging, threads)
+    m.close()
+
+
+def test_host_round_trip_across_128m_slices():
+    """340 MiB over 128 MiB x 2 device slots (4 host slots): snapshots go through a device slot
+    and a DMA, the device ring wraps, and slice edges fall inside entries."""
+    need_gpu()
+    sizes = [(100 << 20) + 7, 13, (150 << 20) + 3 * 4096 + 5, 0, (90 << 20) + 4095]
+    arena, datas = _setup(sizes, seed=52)
+    m, _, _ = _host_round_trip(arena, datas, staging=(128 << 20, 2), threads=16)
+    assert m.image_bytes > 2 * (128 << 20)
+    m.close()
+
+
+def test_host_restore_flags_planted_corruption():
+    need_gpu()
+    arena, datas = _setup(RAGGED, seed=53)
+    m = gms.Manifest(arena.entries)
+    m.set_staging(1 << 20, 2)
+    o_img = oracle.pack(datas)
+    o_blk, _ = oracle.hashes(datas)
+    off, base = m.layout()
+    bad = o_img.copy()
+    spots = [(0, 5), (4, (2 << 20) + 9), (7, 77_776)]  # (entry, byte)
+    want = [d.copy() for d in datas]
+    for e, b in spots:
+        bad[off[e] + b] ^= 0x81
+        want[e][b] ^= 0x81
+    want_cnt, want_lst = oracle.verify(want, o_blk)
+    assert want_cnt == 3 and sorted(int(v) for v in want_lst) == sorted(int(base[e]) + b // 4096 for e, b in spots)
+    cnt, lst = u64_dev(1), u64_dev(4)
+    gms.restore_from_host(m, bad, expected=from_u64(o_blk), mismatch_count=cnt, mismatch_list=lst, mismatch_cap=4)
+    torch.cuda.synchronize()
+    assert to_u64(cnt)[0] == want_cnt
+    assert np.array_equal(np.sort(to_u64(lst, want_cnt)), want_lst)
+    back, _ = arena.read()
+    assert all(np.array_equal(a, b) for a, b in zip(back, want))
+    m.close()
+
+
+def test_image_may_be_reused_when_restore_returns():
+    """The restore has copied every slice out of the image when it returns, although the
+    scatter may still be running: overwriting the image at once changes nothing restored."""
+    need_gpu()
+    arena, datas = _setup([40 << 20, 123_457, 9 << 20], seed=54, misalign=False)
+    m = gms.Manifest(arena.entries)
+    m.set_staging(1 << 20, 2)  # many slices, so the scatter trails the copies
+    src = oracle.pack(datas)
+    arena.poison()
+    gms.restore_from_host(m, src)
+    src[:] = 0xEE
+    torch.cuda.synchronize()
+    back, whole = arena.read()
+    assert all(np.array_equal(a, b) for a, b in zip(back, datas)) and arena.outside_untouched(whole)
+    m.close()
+
+
+def test_host_calls_interleave_with_other_ring_calls(tmp_path):
+    """Pinned restore, host snapshot, file snapshot and host restore on one manifest, issued
+    back to back without synchronizing: the library orders its ring calls."""
+    need_gpu()
+    arena, datas = _setup(RAGGED, seed=55)
+    m = gms.Manifest(arena.entries)
+    m.set_staging(1 << 20, 2)
+    o_img = oracle.pack(datas)
+    pinned = torch.from_numpy(o_img.copy()).pin_memory()
+    arena.poison()
+    gms.restore(m, pinned, m.image_bytes, gms.MEM_HOST_PINNED)
+    out = np.zeros(m.image_bytes, dtype=np.uint8)
+    gms.snapshot_to_host(m, out)
+    assert np.array_equal(out, o_img)
+    path = tmp_path / "img.bin"
+    gms.snapshot_to_file(m, path, flags=0)
+    assert np.array_equal(np.fromfile(path, dtype=np.uint8), o_img)
+    arena.poison()
+    gms.restore_from_host(m, out)
+    torch.cuda.synchronize()
+    back, whole = arena.read()
+    assert all(np.array_equal(a, b) for a, b in zip(back, datas)) and arena.outside_untouched(whole)
+    m.close()
+
+
+def test_host_image_argument_errors():
+    need_gpu()
+    arena, datas = _setup([5000, 300], seed=56)
+    m = gms.Manifest(arena.entries)
+    small = np.zeros(m.image_bytes - 4096, dtype=np.uint8)
+    for call in (lambda: gms.restore_from_host(m, small), lambda: gms.snapshot_to_host(m, small)):
+        with pytest.raises(gms.GmsError) as e:
+            call()
+        assert e.value.status == gms.GMS_ERR_SIZE
+    dev = torch.zeros(m.image_bytes, dtype=torch.uint8, device="cuda")
+    for call in (lambda: gms.restore_from_host(m, dev), lambda: gms.snapshot_to_host(m, dev)):
+        with pytest.raises(gms.GmsError) as e:
+            call()
+        assert e.value.status == gms.GMS_ERR_INVALID
+    with pytest.raises(gms.GmsError) as e:
+        gms.restore_from_host(m, 0, m.image_bytes)
+    assert e.value.status == gms.GMS_ERR_INVALID
+    with pytest.raises(gms.GmsError) as e:
+        gms.restore_from_host(m, np.zeros(m.image_bytes, np.uint8), threads=65)
+    assert e.value.status == gms.GMS_ERR_INVALID
+    with pytest.raises(ValueError):
+        gms.snapshot_to_host(m, np.zeros((2, m.image_bytes), np.uint8)[:, ::2])
+    empty = gms.Manifest([])
+    gms.snapshot_to_host(empty, 0, 0)
+    gms.restore_from_host(empty, 0, 0)
+    # a CPU tensor works as a host image too
+    t = torch.zeros(m.image_bytes, dtype=torch.uint8)
+    gms.snapshot_to_host(m, t)
+    assert np.array_equal(t.numpy(), oracle.pack(datas))
+    empty.close()
+    m.close()
