@@ -22,6 +22,7 @@ import json
 import os
 import statistics
 import sys
+import threading
 import time
 
 ROOT = os.path.dirname(os.path.abspath(__file__))
@@ -98,6 +99,85 @@ class Timer:
         return out
 
 
+class GpuSampler:
+    """Polls the card's clock levels, junction and HBM temperatures and power from sysfs
+    on a thread while a row runs (every 5 ms); the summary is empty where the files are absent."""
+
+    def __init__(self, period: float = 0.005):
+        import glob
+
+        cards = sorted(glob.glob("/sys/class/drm/card*/device/pp_dpm_sclk"))
+        self.dev = os.path.dirname(cards[0]) if cards else None
+        hw = sorted(glob.glob(os.path.join(self.dev, "hwmon", "hwmon*"))) if self.dev else []
+        self.hwmon = hw[0] if hw else None
+        self.period = period
+        self.samples = []
+        self._stop = threading.Event()
+        self._t = None
+
+    @staticmethod
+    def _read(path):
+        try:
+            with open(path) as f:
+                return f.read()
+        except OSError:
+            return None
+
+    def _sample(self):
+        s = {}
+        for clk in ("sclk", "mclk", "fclk", "socclk"):
+            txt = self._read(os.path.join(self.dev, "pp_dpm_" + clk))
+            for line in (txt or "").splitlines():
+                if line.rstrip().endswith("*"):
+                    s[clk + "_mhz"] = int(line.split(":")[1].strip().split("Mhz")[0].split("MHz")[0])
+        if self.hwmon:
+            for key, name, scale in (("junction_c", "temp2_input", 1e3), ("mem_c", "temp3_input", 1e3),
+                                     ("power_w", "power1_input", 1e6)):
+                v = self._read(os.path.join(self.hwmon, name))
+                if v and v.strip().lstrip("-").isdigit():
+                    s[key] = int(v) / scale
+        return s
+
+    def _run(self):
+        while not self._stop.is_set():
+            self.samples.append(self._sample())
+            self._stop.wait(self.period)
+
+    def __enter__(self):
+        if self.dev:
+            self._t = threading.Thread(target=self._run, daemon=True)
+            self._t.start()
+        return self
+
+    def __exit__(self, *exc):
+        self._stop.set()
+        if self._t:
+            self._t.join()
+
+    def summary(self):
+        out = {}
+        for key in ("sclk_mhz", "mclk_mhz", "fclk_mhz", "socclk_mhz", "power_w"):
+            v = [s[key] for s in self.samples if key in s]
+            if v:
+                out[key + "_median"] = statistics.median(v)
+        for key in ("junction_c", "mem_c"):
+            v = [s[key] for s in self.samples if key in s]
+            if v:
+                out[key + "_max"] = max(v)
+        if out:
+            out["samples"] = len(self.samples)
+        return out
+
+
+def settled(timer, fn, warm: int = 3, reps: int = 20):
+    """Median launch time after `warm` untimed launches.  Switching between rows of different
+    VALU load moves the shader clock (about 2.37 GHz under the copy, 2.19 GHz under verify),
+    and the first launches after a switch run at neither."""
+    for _ in range(warm):
+        fn()
+    return statistics.median(timer.run(fn, reps))
+
+
 def build_weights(torch, synth, name):
     seed, specs = synth.weight_set(name)
     tensors = []
@@ -143,6 +223,7 @@ def main():
     gms.snapshot(m, image, m.image_bytes, gms.MEM_DEVICE, blk_hash=expected, ten_hash=ten_hash)
     torch.cuda.synchronize()
     log(f"llama8b: {n} tensors, {P} B, {nb} blocks, {nchunks} chunks; setup {time.time() - t0:.1f}s")
+    pinned_reserved = reserve_pinned(torch, synth, rows, m.image_bytes)
 
     cnt = torch.zeros(1, dtype=torch.int64, device="cuda")
     mlist = torch.zeros(64, dtype=torch.int64, device="cuda")
@@ -164,6 +245,7 @@ def main():
 
     # ---------------------------------------------------------------- main step
     main_times = []
+    gpu_main = None
     if "main" in rows:
         for _ in range(args.warmup):
             fused_restore()
@@ -172,13 +254,14 @@ def main():
         evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
                for _ in range(args.steps)]
         torch.cuda.synchronize()
-        w0 = time.perf_counter()
-        for a, b in evs:
-            a.record(s)
-            fused_restore()
-            b.record(s)
-        torch.cuda.synchronize()
-        wall = time.perf_counter() - w0
+        with GpuSampler() as gpu_main:
+            w0 = time.perf_counter()
+            for a, b in evs:
+                a.record(s)
+                fused_restore()
+                b.record(s)
+            torch.cuda.synchronize()
+            wall = time.perf_counter() - w0
         main_times = [a.elapsed_time(b) / 1e3 for a, b in evs]
         assert int(cnt.item()) == 0
         log(f"fused restore+verify: wall {wall * 1e3 / args.steps:.3f} ms/step, "
@@ -189,20 +272,23 @@ def main():
     # ---------------------------------------------------------------- other rows
     if "snapshot" in rows:
         blk2 = torch.zeros(nb, dtype=torch.int64, device="cuda")
-        ts = timer.run(lambda: gms.snapshot(m, image, m.image_bytes, gms.MEM_DEVICE, blk_hash=blk2), 5)
+        with GpuSampler() as gs:
+            t = settled(timer, lambda: gms.snapshot(m, image, m.image_bytes, gms.MEM_DEVICE, blk_hash=blk2))
         assert torch.equal(blk2, expected)
-        t = statistics.median(ts)
-        result_rows["snapshot_d2d_hash"] = {"s": t, "GB_s": P / t / 1e9, "hbm_frac": 2 * P / t / 1e9 / HBM_PEAK_GBS}
+        result_rows["snapshot_d2d_hash"] = {"s": t, "GB_s": P / t / 1e9, "hbm_frac": 2 * P / t / 1e9 / HBM_PEAK_GBS,
+                                            "gpu": gs.summary()}
     if "plain" in rows:
-        ts = timer.run(lambda: gms.restore(m, image, m.image_bytes, gms.MEM_DEVICE), 5)
-        t = statistics.median(ts)
-        result_rows["restore_d2d_plain"] = {"s": t, "GB_s": P / t / 1e9, "hbm_frac": 2 * P / t / 1e9 / HBM_PEAK_GBS}
+        with GpuSampler() as gs:
+            t = settled(timer, lambda: gms.restore(m, image, m.image_bytes, gms.MEM_DEVICE))
+        result_rows["restore_d2d_plain"] = {"s": t, "GB_s": P / t / 1e9, "hbm_frac": 2 * P / t / 1e9 / HBM_PEAK_GBS,
+                                            "gpu": gs.summary()}
     if "verify" in rows:
         vc = torch.zeros(1, dtype=torch.int64, device="cuda")
-        ts = timer.run(lambda: gms.verify(m, expected=expected, mismatch_count=vc), 5)
+        with GpuSampler() as gs:
+            t = settled(timer, lambda: gms.verify(m, expected=expected, mismatch_count=vc))
         assert int(vc.item()) == 0
-        t = statistics.median(ts)
-        result_rows["verify_only"] = {"s": t, "GB_s": P / t / 1e9, "hbm_frac": P / t / 1e9 / HBM_PEAK_GBS}
+        result_rows["verify_only"] = {"s": t, "GB_s": P / t / 1e9, "hbm_frac": P / t / 1e9 / HBM_PEAK_GBS,
+                                      "gpu": gs.summary()}
     if "sequential" in rows:  # restore, then a separate verify pass: 3P bytes against the fused 2P
         vc = torch.zeros(1, dtype=torch.int64, device="cuda")
 
@@ -210,7 +296,7 @@ def main():
             gms.restore(m, image, m.image_bytes, gms.MEM_DEVICE)
             gms.verify(m, expected=expected, mismatch_count=vc)
 
-        t = statistics.median(timer.run(seq, 5))
+        t = settled(timer, seq, reps=10)
         assert int(vc.item()) == 0
         result_rows["restore_then_verify_sequential"] = {
             "s": t, "GB_s": P / t / 1e9, "hbm_frac": (3 * P + 8 * nb) / t / 1e9 / HBM_PEAK_GBS,
@@ -220,8 +306,7 @@ def main():
     if "copy" in rows:
         a = torch.empty(4 << 30, dtype=torch.uint8, device="cuda")
         b = torch.empty_like(a)
-        ts = timer.run(lambda: b.copy_(a), 5)
-        t = statistics.median(ts)
+        t = settled(timer, lambda: b.copy_(a))
         result_rows["torch_copy_4GiB_reference"] = {"s": t, "hbm_GB_s": 2 * a.numel() / t / 1e9,
                                                     "hbm_frac": 2 * a.numel() / t / 1e9 / HBM_PEAK_GBS}
         del a, b
@@ -233,10 +318,7 @@ def main():
         del a, b
 
     if "h2d" in rows:
-        t0 = time.perf_counter()
-        pinned = torch.empty(m.image_bytes, dtype=torch.uint8, pin_memory=True)
-        pin_s = time.perf_counter() - t0
-        log(f"pinned {m.image_bytes} B in {pin_s:.1f}s")
+        pinned = pinned_view(m.image_bytes)
         # link peak: 1 GiB pinned -> device copies
         gib = pinned[: 1 << 30]
         dst = torch.empty(1 << 30, dtype=torch.uint8, device="cuda")
@@ -253,7 +335,9 @@ def main():
         def h2d():
             gms.restore(m, pinned, m.image_bytes, gms.MEM_HOST_PINNED, expected=expected, mismatch_count=hc)
 
+        h2d_warm = settle_link(timer, h2d, P, link)
         th = statistics.median(timer.run(h2d, 3))
+        link_after = link_now(torch, timer)
         assert int(hc.item()) == 0
         m.set_staging(0, 0)
         tz = statistics.median(timer.run(h2d, 2))
@@ -261,9 +345,10 @@ def main():
         snap_z = statistics.median(timer.run(lambda: gms.snapshot(m, pinned, m.image_bytes, gms.MEM_HOST_PINNED), 2))
         m.set_staging(gms.DEFAULT_SLICE_BYTES, gms.DEFAULT_SLOTS)
         result_rows["h2d"] = {
-            "pinned_alloc_s": pin_s,
+            "pinned_buffer": pinned_reserved,
             "link_peak_GB_s": link,
             "restore_verify_ring_s": th, "restore_verify_ring_GB_s": P / th / 1e9,
+            "restore_untimed_calls_s": h2d_warm, "link_right_after_GB_s": link_after,
             "link_frac": P / th / 1e9 / link,
             "restore_verify_zero_copy_s": tz, "restore_verify_zero_copy_GB_s": P / tz / 1e9,
             "link_peak_d2h_GB_s": link_d2h,
@@ -301,7 +386,8 @@ def main():
         roof = {"bound": "hbm", "kernel": "gms::k_stream<restore,hash>", "achieved": round(achieved, 1),
                 "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
                 "traffic": traffic, "algorithmic_bytes_per_launch": alg,
-                "avg_launch_ms": round(kt * 1e3, 4)}
+                "avg_launch_ms": round(kt * 1e3, 4),
+                "gpu_during_timed_steps": gpu_main.summary() if gpu_main else {}}
 
     # ---------------------------------------------------------------- CPU oracle
     cpu = None
@@ -505,13 +591,12 @@ def bench_kv(torch, np, gms, synth, timer, link=None):
     def run():
         gms.restore(m, img, m.image_bytes, expected=exp, mismatch_count=cnt, mismatch_list=lst, mismatch_cap=8)
 
-    ts = timer.run(run, 7)
+    t = settled(timer, run)
     c = int(cnt.item())
     flagged = sorted(int(v) for v in lst[:min(c, 8)].cpu().tolist())
     # dead units keep the poison
     dead = np.setdiff1d(np.arange(p.blocks), live)
-    dead_ok = all(bool((t.view(p.blocks, p.unit_bytes)[torch.from_numpy(dead).cuda()] == 0xA5).all()) for t in pool[:4])
-    t = statistics.median(ts)
+    dead_ok = all(bool((u.view(p.blocks, p.unit_bytes)[torch.from_numpy(dead).cuda()] == 0xA5).all()) for u in pool[:4])
     h2d = h2d_leg(torch, gms, timer, m, img, exp, link)  # the same planted flip, through the host link
     return {"entries": m.num_entries, "payload_bytes": P, "s": t, "GB_s": P / t / 1e9,
             "hbm_frac": 2 * P / t / 1e9 / HBM_PEAK_GBS, "mismatches": c, "flagged": flagged,
@@ -519,6 +604,64 @@ def bench_kv(torch, np, gms, synth, timer, link=None):
 
 
 H2D_MAX_PINNED = 64 << 30  # the measuring host cannot pin the 122 GB MoE image
+# One pinned host buffer serves every pinned-image leg.  It is allocated before anything else
+# has churned host memory: a 17.6 GB pinned buffer allocated late in a run, after some hundred GB
+# of host allocations had come and gone, fed the DMA at 59 to 91% of the link instead of 99%.
+_PINNED = {"buf": None}
+
+
+def link_now(torch, timer, reps: int = 3):
+    """A plain 1 GiB pinned-to-device copy, to put a leg's rate beside what the link gives at that
+    moment (the host link of the measuring machine sometimes runs at half its rate for seconds)."""
+    buf = _PINNED["buf"]
+    if buf is None or buf.numel() < (1 << 30):
+        return None
+    dst = torch.empty(1 << 30, dtype=torch.uint8, device="cuda")
+    t = statistics.median(timer.run(lambda: dst.copy_(buf[: 1 << 30], non_blocking=True), reps))
+    del dst
+    return round((1 << 30) / t / 1e9, 2)
+
+
+def settle_link(timer, run, payload, link, max_calls: int = 10):
+    """Untimed calls until one reaches 90% of `link` (or, with no link figure, until two in a
+    row agree within 2%), at most `max_calls`; returns every call time."""
+    calls = [statistics.median(timer.run(run, 1))]
+    while len(calls) < max_calls:
+        if link and payload / calls[-1] / 1e9 >= 0.9 * link:
+            break
+        calls += timer.run(run, 1)
+        if not link and abs(calls[-1] - calls[-2]) <= 0.02 * calls[-1]:
+            break
+    return [round(x, 4) for x in calls]
+
+
+def image_bytes_of(sizes):
+    return sum((n + 4095) // 4096 * 4096 for n in sizes)
+
+
+def reserve_pinned(torch, synth, rows, llama_image_bytes):
+    """Allocates the pinned buffer for the largest image a pinned leg of `rows` will copy."""
+    need = [llama_image_bytes] if "h2d" in rows else []
+    if "kv" in rows:
+        p = synth.kv_pool()
+        need.append(p.layers * p.n_live * p.unit_bytes)
+    if "shards" in rows:
+        need += [image_bytes_of(sp.nbytes for sp in synth.weight_set(n)[1]) for n in ("llama70b_tp8", "moe")]
+    need = [n for n in need if n <= H2D_MAX_PINNED]
+    if not need:
+        return None
+    t0 = time.perf_counter()
+    _PINNED["buf"] = torch.empty(max(need), dtype=torch.uint8, pin_memory=True)
+    dt = time.perf_counter() - t0
+    log(f"pinned {max(need)} B for the pinned-image legs in {dt:.1f}s")
+    return {"bytes": max(need), "alloc_s": round(dt, 3)}
+
+
+def pinned_view(nbytes):
+    buf = _PINNED["buf"]
+    if buf is None or buf.numel() < nbytes:
+        raise RuntimeError("no pinned buffer reserved for this image")
+    return buf[:nbytes]
 
 
 def pageable_leg(torch, np, gms, timer, m, exp, link=None, link_d2h=None, reps=3):
@@ -552,32 +695,30 @@ def pageable_leg(torch, np, gms, timer, m, exp, link=None, link_d2h=None, reps=3
 
 
 def h2d_leg(torch, gms, timer, m, img, exp, link=None, reps=3, cap=8):
-    """The same restore+verify from a pinned host copy of the image, through the staging ring:
-    pinning time (not timed in the rate), rate, and the mismatches it reports.  One untimed
-    call first allocates the manifest's staging ring.  An image this host cannot pin is
-    restored from pageable host memory instead."""
+    """The same restore+verify from a pinned host copy of the image (in the buffer reserved at
+    start-up), through the staging ring: rate, and the mismatches it reports.  One untimed call
+    first allocates the manifest's staging ring.  An image this host cannot pin is restored from
+    pageable host memory instead."""
     if m.image_bytes > H2D_MAX_PINNED:
         import numpy as np
 
         out = pageable_leg(torch, np, gms, timer, m, exp, link)
         out["source"] = f"pageable host memory: this host cannot pin an image of {m.image_bytes} B"
         return out
-    t0 = time.perf_counter()
-    pinned = torch.empty(m.image_bytes, dtype=torch.uint8, pin_memory=True)
-    pin_s = time.perf_counter() - t0
+    pinned = pinned_view(m.image_bytes)
     pinned.copy_(img)
     cnt = torch.zeros(1, dtype=torch.int64, device="cuda")
     lst = torch.zeros(cap, dtype=torch.int64, device="cuda")
     run = lambda: gms.restore(m, pinned, m.image_bytes, gms.MEM_HOST_PINNED, expected=exp, mismatch_count=cnt,
                               mismatch_list=lst, mismatch_cap=cap)
-    run()
+    warm = settle_link(timer, run, m.payload_bytes, link)
     t = statistics.median(timer.run(run, reps))
     c = int(cnt.item())
-    out = {"pinned_alloc_s": round(pin_s, 3), "restore_verify_s": t, "restore_verify_GB_s": m.payload_bytes / t / 1e9,
+    out = {"restore_verify_s": t, "restore_verify_GB_s": m.payload_bytes / t / 1e9,
+           "untimed_calls_s": warm, "link_right_after_GB_s": link_now(torch, timer),
            "mismatches": c, "flagged": sorted(int(v) for v in lst[:min(c, cap)].cpu().tolist())}
     if link:
         out["link_frac"] = m.payload_bytes / t / 1e9 / link
-    del pinned
     return out
 
 
@@ -594,9 +735,8 @@ def bench_shard(torch, gms, synth, timer, name, link=None):
     exp = torch.zeros(m.num_blocks, dtype=torch.int64, device="cuda")
     gms.snapshot(m, img, m.image_bytes, blk_hash=exp)
     cnt = torch.zeros(1, dtype=torch.int64, device="cuda")
-    ts = timer.run(lambda: gms.restore(m, img, m.image_bytes, expected=exp, mismatch_count=cnt), 5)
+    t = settled(timer, lambda: gms.restore(m, img, m.image_bytes, expected=exp, mismatch_count=cnt))
     assert int(cnt.item()) == 0
-    t = statistics.median(ts)
     out = {"tensors": len(tensors), "payload_bytes": P, "chunks": m.num_chunks, "restore_verify_s": t,
            "restore_verify_GB_s": P / t / 1e9, "hbm_frac": (2 * P + 8 * m.num_blocks) / t / 1e9 / HBM_PEAK_GBS}
     log(f"{name}: restore+verify {t * 1e3:.2f} ms, {out['hbm_frac'] * 100:.1f}% of HBM peak")
@@ -677,9 +817,8 @@ def bench_kv_vmm(torch, np, gms, synth, timer):
         pool.remap(kv[0], span)
         t_map = time.perf_counter() - t0
         cnt = torch.zeros(1, dtype=torch.int64, device="cuda")
-        ts = timer.run(lambda: gms.restore(m, img, m.image_bytes, expected=exp, mismatch_count=cnt), 5)
+        t = settled(timer, lambda: gms.restore(m, img, m.image_bytes, expected=exp, mismatch_count=cnt))
         assert int(cnt.item()) == 0
-        t = statistics.median(ts)
         payload = m.payload_bytes
         m.close()
         return {"pool_bytes": span, "release_s": t_rel, "remap_s": t_map, "restore_verify_s": t,
