@@ -2,8 +2,9 @@
  * C99 client of include/gms.h on the GPU, with no Python or torch: device
  * memory from hipMalloc, streams as plain HIP handles.  Snapshot, restore and
  * verify results are compared with the C oracle (linked beside the library,
- * sharing nothing with it) on the same host bytes; the model-state store is
- * driven through one commit and one verified read-only lease.  Exits non-zero
+ * sharing nothing with it) on the same host bytes, for device images and for a
+ * pageable host image; the model-state store is driven through one commit and
+ * one verified read-only lease.  Exits non-zero
  * on the first failed check, printing it.
  */
 #include <stdint.h>
@@ -104,6 +105,27 @@ int main(void)
     CHECK(hipMemcpy(&cnt, d_cnt, 8, hipMemcpyDeviceToHost) == hipSuccess && cnt == 1);
     CHECK(hipMemcpy(list, d_list, 8, hipMemcpyDeviceToHost) == hipSuccess && list[0] == base[3] + 2);
     CHECK(gms_verify(m, NULL, NULL, NULL, NULL, NULL, 0, s) == GMS_ERR_INVALID); /* nothing to do */
+
+    /* pageable host image: snapshot into malloc'd memory, then restore from it with the oracle's hashes */
+    uint8_t *h_img = malloc(ib);
+    CHECK(h_img);
+    memset(h_img, 0xEE, ib);
+    CHECK(hipMemcpy(dev[3] + mis[3] + 2 * 4096 + 50, &host[3][2 * 4096 + 50], 1, hipMemcpyHostToDevice) == hipSuccess);
+    CHECK(gms_snapshot_to_host(m, h_img, ib, 3, d_blk, NULL, s) == GMS_OK);
+    CHECK(memcmp(h_img, o_img, ib) == 0);
+    CHECK(hipMemcpy(g_blk, d_blk, nb * 8, hipMemcpyDeviceToHost) == hipSuccess && memcmp(g_blk, o_blk, nb * 8) == 0);
+    for (int i = 0; i < N; ++i) CHECK(hipMemset(dev[i] + mis[i], 0x33, sizes[i]) == hipSuccess);
+    CHECK(gms_restore_from_host(m, h_img, ib, 0, d_exp, NULL, NULL, d_cnt, d_list, 8, s) == GMS_OK);
+    memset(h_img, 0, ib); /* the image may be reused once the call returns */
+    CHECK(hipStreamSynchronize(s) == hipSuccess);
+    CHECK(hipMemcpy(&cnt, d_cnt, 8, hipMemcpyDeviceToHost) == hipSuccess && cnt == 0);
+    for (int i = 0; i < N; ++i) {
+        CHECK(hipMemcpy(back[i], dev[i] + mis[i], sizes[i], hipMemcpyDeviceToHost) == hipSuccess);
+        CHECK(memcmp(back[i], host[i], sizes[i]) == 0);
+    }
+    CHECK(gms_restore_from_host(m, h_img, ib - 1, 0, NULL, NULL, NULL, NULL, NULL, 0, s) == GMS_ERR_SIZE);
+    CHECK(gms_snapshot_to_host(m, d_img, ib, 0, NULL, NULL, s) == GMS_ERR_INVALID); /* device memory */
+    free(h_img);
 
     /* the model-state store: populate, commit, verified read-only lease */
     gms_store *st = NULL;
