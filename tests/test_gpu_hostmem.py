@@ -177,3 +177,58 @@ def test_host_image_argument_errors():
     assert np.array_equal(t.numpy(), oracle.pack(datas))
     empty.close()
     m.close()
+
+
+def test_concurrent_host_threads_on_separate_manifests(tmp_path):
+    """Four host threads, each with its own manifest and stream, run pageable-host, file and
+    pinned-ring round trips at the same time (ctypes releases the GIL, so the library's worker
+    pools, rings and per-thread error state all overlap); every result equals the oracle."""
+    import threading
+
+    need_gpu()
+    setups = []
+    for k in range(4):
+        sizes = [int(v) for v in np.random.default_rng(70 + k).integers(1, 3 << 20, 6)] + [4096 * (k + 1), 13]
+        arena, datas = _setup(sizes, seed=70 + k)
+        m = gms.Manifest(arena.entries)
+        m.set_staging((1 + k) << 20, 2)
+        setups.append((arena, datas, m, torch.cuda.Stream()))
+    torch.cuda.synchronize()
+    errors, results = [], {}
+
+    def work(k):
+        try:
+            arena, datas, m, st = setups[k]
+            o_img = oracle.pack(datas)
+            o_blk, _ = oracle.hashes(datas)
+            exp = from_u64(o_blk)
+            cnt = u64_dev(1)
+            img = np.zeros(m.image_bytes, dtype=np.uint8)
+            for rep in range(3):
+                gms.snapshot_to_host(m, img, stream=st)
+                assert np.array_equal(img, o_img), f"thread {k}: host snapshot"
+                gms.restore_from_host(m, img, expected=exp, mismatch_count=cnt, stream=st)
+                path = tmp_path / f"t{k}.img"
+                gms.snapshot_to_file(m, path, flags=0, stream=st)
+                gms.restore_from_file(m, path, flags=0, expected=exp, mismatch_count=cnt, stream=st)
+                pinned = torch.from_numpy(o_img.copy()).pin_memory()
+                gms.restore(m, pinned, m.image_bytes, gms.MEM_HOST_PINNED, expected=exp, mismatch_count=cnt,
+                            stream=st)
+                st.synchronize()
+                results[(k, rep)] = int(to_u64(cnt)[0])
+                with pytest.raises(gms.GmsError):  # a failing call in one thread leaves the others alone
+                    gms.restore_from_host(m, img, m.image_bytes - 1, stream=st)
+        except BaseException as e:  # reported by the main thread
+            errors.append((k, repr(e)))
+
+    threads = [threading.Thread(target=work, args=(k,)) for k in range(4)]
+    for t in threads:
+        t.start()
+    for t in threads:
+        t.join()
+    assert not errors, errors
+    assert all(v == 0 for v in results.values()) and len(results) == 12
+    for arena, datas, m, _ in setups:
+        back, whole = arena.read()
+        assert all(np.array_equal(a, b) for a, b in zip(back, datas)) and arena.outside_untouched(whole)
+        m.close()
