@@ -36,7 +36,11 @@ ALL_ROWS = ["main", "snapshot", "plain", "verify", "sequential", "tiny", "h2d", 
 # header's block and default chunk sizes and the chunking in manifest creation.
 KERNEL_SOURCES = ["paper_2609_25451_amd/csrc/gms_kernels.hip", "paper_2609_25451_amd/csrc/gms_internal.h"]
 HEADER = "include/gms.h"
-CHUNKING = ("paper_2609_25451_amd/csrc/gms_api.hip", "int gms_manifest_create(")
+# the host code that decides what the measured kernel is launched over: the chunking, the launch
+# groups and the launch itself (function bodies), and the grouping threshold (a line)
+CHUNKING = ("paper_2609_25451_amd/csrc/gms_api.hip",
+            ["int gms_manifest_create(", "uint32_t unit_class(", "void plan_launch_groups(", "hipError_t launch_all("],
+            ["constexpr uint64_t kSplitUnits"])
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_restore_verify_llama8b.json")
 
 
@@ -63,8 +67,11 @@ def kernel_source_digest() -> str:
                  .encode())
     with open(os.path.join(ROOT, CHUNKING[0])) as f:
         src = f.read()
-    start = src.index(CHUNKING[1])
-    h.update(_code(src[start:src.index("\n}\n", start)]).encode())
+    for marker in CHUNKING[1]:
+        start = src.index(marker)
+        h.update(_code(src[start:src.index("\n}\n", start)]).encode())
+    for prefix in CHUNKING[2]:
+        h.update("".join(l for l in src.splitlines(True) if l.startswith(prefix)).encode())
     return h.hexdigest()[:16]
 
 

@@ -146,6 +146,11 @@ uint64_t gms_payload_bytes(const gms_manifest *m); /* sum of n_i                
 uint64_t gms_image_bytes(const gms_manifest *m);   /* sum of roundup(n_i, 4096)  */
 uint64_t gms_num_blocks(const gms_manifest *m);    /* sum of ceil(n_i / 4096)    */
 uint64_t gms_num_chunks(const gms_manifest *m);    /* work items                 */
+/* Kernel launches per data-plane call on a device image.  Chunks that need
+ * far fewer work units than the largest (tiny entries beside large ones) are
+ * launched apart once the idle units they would otherwise leave outweigh a
+ * launch; a manifest of similar chunks is one launch. */
+uint64_t gms_num_launch_groups(const gms_manifest *m);
 int gms_manifest_device(const gms_manifest *m);
 
 /* Copies img_off[n] and blk_base[n] (host arrays; either may be NULL). */
@@ -161,8 +166,8 @@ int gms_layout(const gms_manifest *m, uint64_t *img_off, uint64_t *blk_base);
  * way: the gather kernel fills a slot on the caller's stream and the copy
  * stream DMAs it to the host image; with slots == 0, or slices below 128 MiB
  * (where the device-to-host DMA loses half the link and more), it writes the
- * image zero-copy.  The image-file calls also use the ring (and a pinned host ring
- * of twice the slots) and need slots > 0.  slice_bytes is 0, which selects
+ * image zero-copy.  The image-file and host-image calls also use the ring (and
+ * a pinned host ring of twice the slots) and need slots > 0.  slice_bytes is 0, which selects
  * GMS_DEFAULT_SLICE_BYTES, or in [4096, 64 GiB]; slots at most 16; a new manifest starts with GMS_DEFAULT_SLICE_BYTES x
  * GMS_DEFAULT_SLOTS (256 MiB slices keep the host link at about 99% of its
  * peak; 64 MiB slices reach about 97.5%).  Takes effect at the next ring
@@ -271,8 +276,8 @@ int gms_snapshot_to_file(const gms_manifest *m, const char *path, uint32_t flags
  * for an empty layout); the library cannot check pageable memory beyond
  * that, so a shorter or unmapped buffer is undefined behaviour.  Device
  * memory is refused (GMS_ERR_INVALID: use gms_restore / gms_snapshot).
- * Errors: GMS_ERR_STATE (host-only manifest, or `stream` capturing a graph),
- * GMS_ERR_INVALID, GMS_ERR_SIZE (image_bytes below the layout), GMS_ERR_HIP,
+ * Errors: GMS_ERR_STATE (host-only manifest, no staging slots, or `stream`
+ * capturing a graph), GMS_ERR_INVALID, GMS_ERR_SIZE (image_bytes below the layout), GMS_ERR_HIP,
  * GMS_ERR_NOMEM (staging rings).
  */
 int gms_restore_from_host(const gms_manifest *m, const void *image, uint64_t image_bytes, uint32_t threads,

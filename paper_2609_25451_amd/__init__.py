@@ -74,6 +74,7 @@ _payload = _sig("gms_payload_bytes", U64, [VP])
 _image_bytes = _sig("gms_image_bytes", U64, [VP])
 _num_blocks = _sig("gms_num_blocks", U64, [VP])
 _num_chunks = _sig("gms_num_chunks", U64, [VP])
+_num_groups = _sig("gms_num_launch_groups", U64, [VP])
 _device = _sig("gms_manifest_device", INT, [VP])
 _layout = _sig("gms_layout", INT, [VP, VP, VP])
 _set_staging = _sig("gms_manifest_set_staging", INT, [VP, U64, ctypes.c_uint32])
@@ -252,6 +253,10 @@ class Manifest:
     @property
     def num_chunks(self) -> int:
         return int(_num_chunks(self._h))
+
+    @property
+    def num_launch_groups(self) -> int:
+        return int(_num_groups(self._h))
 
     @property
     def device(self) -> int:

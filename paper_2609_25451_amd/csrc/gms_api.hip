@@ -107,15 +107,85 @@ int ensure_ring(gms_manifest *m)
         return free_ring(m), fail_hip(e, "staging ring: hipEventCreate");
     m->ring_slice = slice;
     m->ring_slots = m->slots;
-    // chunk ranges per slice; chunks never straddle a slice (slice % chunk == 0)
+    // chunk ranges per group and slice; chunks never straddle a slice
+    // (slice % chunk == 0) and are in image order within a group
     const uint64_t nslices = ceil_div(m->image_bytes, slice);
-    m->slice_first.assign(nslices + 1, m->chunks.size());
-    uint64_t ci = 0;
-    for (uint64_t s = 0; s < nslices; ++s) {
-        while (ci < m->chunks.size() && m->chunks[ci].img < s * slice) ++ci;
-        m->slice_first[s] = ci;
+    m->slice_first.assign(m->groups.size() * (nslices + 1), 0);
+    for (size_t g = 0; g < m->groups.size(); ++g) {
+        const gms::LaunchGroup &lg = m->groups[g];
+        uint64_t ci = lg.first;
+        for (uint64_t s = 0; s < nslices; ++s) {
+            while (ci < lg.first + lg.count && m->chunks[ci].img < s * slice) ++ci;
+            m->slice_first[g * (nslices + 1) + s] = ci;
+        }
+        m->slice_first[g * (nslices + 1) + nslices] = lg.first + lg.count;
     }
     return GMS_OK;
+}
+
+// Work units a chunk needs as a power of two: the smallest s with 2^s units of
+// kBlocksPerUnit blocks covering it.
+uint32_t unit_class(uint32_t len)
+{
+    const uint64_t units = ceil_div(ceil_div(len, kBlockBytes), kBlocksPerUnit);
+    uint32_t s = 0;
+    while ((1ull << s) < units) ++s;
+    return s;
+}
+
+// Idle work units that justify one more launch: an idle workgroup costs about
+// 0.7 ns of the whole chip (measured: 1.4 M of them added 1.0 ms to a restore),
+// a launch some microseconds.
+constexpr uint64_t kSplitUnits = 16384;
+
+void plan_launch_groups(gms_manifest *m)
+{
+    // One launch covers a set of chunks with the units of the largest, so a
+    // chunk that needs fewer units leaves the rest idle.  Walking the classes
+    // from the largest down, a class gets a launch of its own (shared with the
+    // smaller classes after it) once the idle units it would leave reach
+    // kSplitUnits; a manifest of similar chunks stays one launch.
+    uint64_t count[kMaxUnitShift + 1] = {};
+    for (const Chunk &c : m->chunks) ++count[unit_class(c.len)];
+    uint32_t group_of[kMaxUnitShift + 1] = {};
+    int top = kMaxUnitShift;
+    while (top > 0 && count[top] == 0) --top;
+    uint32_t g = (uint32_t)top;
+    for (int s = top; s >= 0; --s) {
+        if (count[s] && (uint32_t)s < g && count[s] * ((1ull << g) - (1ull << s)) >= kSplitUnits) g = (uint32_t)s;
+        group_of[s] = g;
+    }
+    // chunks by group (larger shift first), in image order within a group
+    std::stable_sort(m->chunks.begin(), m->chunks.end(), [&](const Chunk &a, const Chunk &b) {
+        return group_of[unit_class(a.len)] > group_of[unit_class(b.len)];
+    });
+    m->groups.clear();
+    for (uint64_t i = 0; i < m->chunks.size(); ++i) {
+        const uint32_t sh = group_of[unit_class(m->chunks[i].len)];
+        if (m->groups.empty() || m->groups.back().shift != sh) m->groups.push_back(LaunchGroup{i, 0, sh});
+        ++m->groups.back().count;
+    }
+}
+
+hipError_t launch_all(const gms_manifest *m, int op, const HashOut &h, uint8_t *img_base, hipStream_t s)
+{
+    for (const LaunchGroup &g : m->groups) {
+        hipError_t e = launch_stream(op, h.any(), m->d_chunks, g.first, g.count, g.shift, img_base, 0, h, s);
+        if (e != hipSuccess) return e;
+    }
+    return hipSuccess;
+}
+
+hipError_t launch_slice(const gms_manifest *m, int op, const HashOut &h, uint64_t sl, uint8_t *slot, hipStream_t s)
+{
+    const uint64_t stride = ceil_div(m->image_bytes, m->ring_slice) + 1;
+    for (size_t g = 0; g < m->groups.size(); ++g) {
+        const uint64_t c0 = m->slice_first[g * stride + sl], c1 = m->slice_first[g * stride + sl + 1];
+        hipError_t e =
+            launch_stream(op, h.any(), m->d_chunks, c0, c1 - c0, m->groups[g].shift, slot, sl * m->ring_slice, h, s);
+        if (e != hipSuccess) return e;
+    }
+    return hipSuccess;
 }
 
 int refuse_capture(hipStream_t s, const char *what)
@@ -131,7 +201,7 @@ int ensure_host_ring(gms_manifest *m)
 {
     int rc = ensure_ring(m);
     if (rc != GMS_OK) return rc;
-    if (!m->d_ring) return fail(GMS_ERR_STATE, "file paths need the staging ring (slots > 0)");
+    if (!m->d_ring) return fail(GMS_ERR_STATE, "image-file and host-image calls need the staging ring (slots > 0)");
     if (m->h_ring) return GMS_OK;
     const uint32_t hk = std::min<uint32_t>(kMaxSlots, 2 * m->ring_slots);
     hipError_t e = hipHostMalloc((void **)&m->h_ring, m->ring_slice * hk, hipHostMallocDefault);
@@ -262,7 +332,7 @@ using gms::ensure_ring;
 // Device-resident image, or zero-copy access to a pinned one: one launch.
 int run_direct(const gms_manifest *m, int op, uint8_t *image, const HashOut &h, hipStream_t s)
 {
-    hipError_t e = gms::launch_stream(op, h.any(), m->d_chunks, 0, m->chunks.size(), m->max_chunk, image, 0, h, s);
+    hipError_t e = gms::launch_all(m, op, h, image, s);
     return e == hipSuccess ? GMS_OK : fail_hip(e, "kernel launch");
 }
 
@@ -299,10 +369,9 @@ int run_ring(gms_manifest *m, int op, const HashOut &h, uint8_t *host_image, hip
         uint8_t *dev = m->d_ring + (uint64_t)slot * slice;
         const uint64_t lo = sl * slice;
         const uint64_t bytes = std::min(slice, m->image_bytes - lo);
-        const uint64_t c0 = m->slice_first[sl], c1 = m->slice_first[sl + 1];
         if (sl >= k) GMS_TRY(hipStreamWaitEvent(producer, m->ev_free[slot], 0));
         if (to_host)
-            GMS_TRY(gms::launch_stream(op, h.any(), m->d_chunks, c0, c1 - c0, m->max_chunk, dev, lo, h, s));
+            GMS_TRY(gms::launch_slice(m, op, h, sl, dev, s));
         else
             GMS_TRY(hipMemcpyAsync(dev, host_image + lo, bytes, hipMemcpyHostToDevice, m->copy_stream));
         GMS_TRY(hipEventRecord(m->ev_filled[slot], producer));
@@ -310,7 +379,7 @@ int run_ring(gms_manifest *m, int op, const HashOut &h, uint8_t *host_image, hip
         if (to_host)
             GMS_TRY(hipMemcpyAsync(host_image + lo, dev, bytes, hipMemcpyDeviceToHost, m->copy_stream));
         else
-            GMS_TRY(gms::launch_stream(op, h.any(), m->d_chunks, c0, c1 - c0, m->max_chunk, dev, lo, h, s));
+            GMS_TRY(gms::launch_slice(m, op, h, sl, dev, s));
         GMS_TRY(hipEventRecord(m->ev_free[slot], consumer));
     }
     // the call ends on the caller's stream once the last slot is consumed
@@ -463,13 +532,13 @@ int gms_manifest_create(const gms_entry *entries, uint64_t n, int device, uint64
                 c.len = (uint32_t)len;
                 c.entry = (uint32_t)i;
                 m->chunks.push_back(c);
-                m->max_chunk = std::max(m->max_chunk, len);
                 pos += len;
             }
             off += ceil_div(nb, GMS_BLOCK_BYTES) * GMS_BLOCK_BYTES;
         }
         m->image_bytes = off;
         m->num_blocks = off / GMS_BLOCK_BYTES;
+        gms::plan_launch_groups(m);
     } catch (const std::bad_alloc &) {
         delete m;
         return fail(GMS_ERR_NOMEM, "manifest tables");
@@ -516,6 +585,7 @@ uint64_t gms_payload_bytes(const gms_manifest *m) { return m ? m->payload : 0; }
 uint64_t gms_image_bytes(const gms_manifest *m) { return m ? m->image_bytes : 0; }
 uint64_t gms_num_blocks(const gms_manifest *m) { return m ? m->num_blocks : 0; }
 uint64_t gms_num_chunks(const gms_manifest *m) { return m ? (uint64_t)m->chunks.size() : 0; }
+uint64_t gms_num_launch_groups(const gms_manifest *m) { return m ? (uint64_t)m->groups.size() : 0; }
 int gms_manifest_device(const gms_manifest *m) { return m ? m->device : GMS_HOST_ONLY; }
 
 int gms_layout(const gms_manifest *m, uint64_t *img_off, uint64_t *blk_base)

@@ -49,14 +49,23 @@ struct DeviceGuard {
 
 }  // namespace gms
 
+namespace gms {
+// Chunks launched together: chunks[first, first + count), each needing at most
+// 2^shift work units.
+struct LaunchGroup {
+    uint64_t first = 0, count = 0;
+    uint32_t shift = 0;
+};
+}  // namespace gms
+
 struct gms_manifest {
     int device = GMS_HOST_ONLY;
     uint64_t n = 0;
     uint64_t chunk_bytes = 0;
-    uint64_t max_chunk = 0;  // longest chunk: sizes the kernel's work units
     uint64_t payload = 0, image_bytes = 0, num_blocks = 0;
     std::vector<uint64_t> img_off;
-    std::vector<gms::Chunk> chunks;  // host copy, sorted by image offset
+    std::vector<gms::Chunk> chunks;  // host copy: by launch group, then by image offset
+    std::vector<gms::LaunchGroup> groups;
     gms::Chunk *d_chunks = nullptr;
 
     // staging rings, created lazily: device slots for pinned-host images, and
@@ -76,7 +85,9 @@ struct gms_manifest {
     hipEvent_t ev_entry = nullptr;
     hipEvent_t ev_done = nullptr;
     bool done_recorded = false;
-    std::vector<uint64_t> slice_first;  // per slice: first chunk index; back() = #chunks
+    // per launch group g and ring slice s, the first chunk of g at or after the
+    // slice's start, at [g * (nslices + 1) + s]; s = nslices gives the group's end
+    std::vector<uint64_t> slice_first;
 };
 
 namespace gms {
@@ -92,6 +103,10 @@ int ensure_ring(gms_manifest *m);       // device slots, copy stream, events, sl
 int ensure_host_ring(gms_manifest *m);  // plus pinned host slots
 int check_common(const gms_manifest *m, const void *image, uint64_t image_bytes, int kind, bool need_image);
 int check_outputs(const gms_manifest *m, const HashOut &h);
+// `op` over every chunk (one launch per group), image byte x at img_base + x.
+hipError_t launch_all(const gms_manifest *m, int op, const HashOut &h, uint8_t *img_base, hipStream_t s);
+// `op` over the chunks of ring slice `sl`, image byte x at slot + (x - sl * ring_slice).
+hipError_t launch_slice(const gms_manifest *m, int op, const HashOut &h, uint64_t sl, uint8_t *slot, hipStream_t s);
 // GMS_ERR_STATE if `s` is capturing a graph: for calls that synchronize or
 // order themselves with library-owned streams and events.
 int refuse_capture(hipStream_t s, const char *what);

@@ -356,9 +356,7 @@ int restore_pipeline(gms_manifest *m, const HostImage &src, const HashOut &h, un
             (e = hipEventRecord(m->ev_host[hslot], m->copy_stream)) != hipSuccess ||
             (e = hipEventRecord(m->ev_filled[slot], m->copy_stream)) != hipSuccess ||
             (e = hipStreamWaitEvent(s, m->ev_filled[slot], 0)) != hipSuccess ||
-            (e = gms::launch_stream(gms::kRestore, h.any(), m->d_chunks, m->slice_first[sl],
-                                    m->slice_first[sl + 1] - m->slice_first[sl], m->max_chunk, dev, lo, h, s)) !=
-                hipSuccess ||
+            (e = gms::launch_slice(m, gms::kRestore, h, sl, dev, s)) != hipSuccess ||
             (e = hipEventRecord(m->ev_free[slot], s)) != hipSuccess) {
             rc = fail_hip(e, "host restore slice");
             break;
@@ -391,18 +389,16 @@ int snapshot_pipeline(gms_manifest *m, const HostImage &dst, const HashOut &h, u
 
     auto enqueue = [&](uint64_t sl) -> int {
         const uint32_t hslot = (uint32_t)(sl % hk);
-        const uint64_t c0 = m->slice_first[sl], c1 = m->slice_first[sl + 1];
         const uint64_t lo = sl * slice;
         if (!via_device) {
-            GMS_TRY(gms::launch_stream(gms::kSnapshot, h.any(), m->d_chunks, c0, c1 - c0, m->max_chunk,
-                                       h_dev + (uint64_t)hslot * slice, lo, h, s));
+            GMS_TRY(gms::launch_slice(m, gms::kSnapshot, h, sl, h_dev + (uint64_t)hslot * slice, s));
             GMS_TRY(hipEventRecord(m->ev_host[hslot], s));
             return GMS_OK;
         }
         const uint32_t slot = (uint32_t)(sl % k);
         uint8_t *dev = m->d_ring + (uint64_t)slot * slice;
         if (sl >= k) GMS_TRY(hipStreamWaitEvent(s, m->ev_free[slot], 0));
-        GMS_TRY(gms::launch_stream(gms::kSnapshot, h.any(), m->d_chunks, c0, c1 - c0, m->max_chunk, dev, lo, h, s));
+        GMS_TRY(gms::launch_slice(m, gms::kSnapshot, h, sl, dev, s));
         GMS_TRY(hipEventRecord(m->ev_filled[slot], s));
         GMS_TRY(hipStreamWaitEvent(m->copy_stream, m->ev_filled[slot], 0));
         GMS_TRY(hipMemcpyAsync(m->h_ring + (uint64_t)hslot * slice, dev, std::min(slice, m->image_bytes - lo),

@@ -8,6 +8,8 @@
 namespace gms {
 
 constexpr uint32_t kBlockBytes = 4096;  // hash block and image alignment
+constexpr uint32_t kBlocksPerUnit = 2;  // 4 KiB blocks per work unit (one per wave of a workgroup)
+constexpr uint32_t kMaxUnitShift = 13;  // a 64 MiB chunk needs 2^13 units
 
 // An entry of the work list: a piece of one entry that never crosses an image
 // offset that is a multiple of the manifest's chunk size.
@@ -35,11 +37,12 @@ struct HashOut {
 // Zeroes the tensor-hash array and the mismatch counter (either may be null).
 hipError_t launch_prologue(const HashOut &h, uint64_t n_entries, hipStream_t s);
 
-// Runs `op` over chunks[first, first + count), none longer than `chunk_bytes`
-// (the manifest's longest chunk sizes the kernel's work units).  The image byte at offset x lives at
-// img_base + (x - img_origin).  `hash` selects the hashing variant.
+// Runs `op` over chunks[first, first + count), each of which needs at most
+// 2^unit_shift work units of kBlocksPerUnit blocks (unit_shift <= kMaxUnitShift).
+// The image byte at offset x lives at img_base + (x - img_origin).  `hash`
+// selects the hashing variant.
 hipError_t launch_stream(int op, bool hash, const Chunk *chunks, uint64_t first, uint64_t count,
-                         uint64_t chunk_bytes, uint8_t *img_base, uint64_t img_origin, const HashOut &h,
+                         uint32_t unit_shift, uint8_t *img_base, uint64_t img_origin, const HashOut &h,
                          hipStream_t s);
 
 }  // namespace gms

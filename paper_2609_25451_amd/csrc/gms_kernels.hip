@@ -34,7 +34,7 @@ constexpr uint64_t kMulA = 0xBF58476D1CE4E5B9ull;
 constexpr uint64_t kMulB = 0x94D049BB133111EBull;
 constexpr uint64_t kSegStrideG = 128ull * kG;    // word-index step between a lane's segments
 constexpr uint64_t kBlockStrideG = 512ull * kG;  // word-index step between blocks
-constexpr int kWaves = 2;                        // waves per workgroup, one block each
+constexpr int kWaves = kBlocksPerUnit;           // waves per workgroup, one block each
 constexpr int kUnitThreads = kWaves * 64;
 constexpr uint32_t kXcds = 8;                    // accelerator complex dies on MI355X
 
@@ -311,15 +311,10 @@ hipError_t launch_prologue(const HashOut &h, uint64_t n_entries, hipStream_t s)
 }
 
 hipError_t launch_stream(int op, bool hash, const Chunk *chunks, uint64_t first, uint64_t count,
-                         uint64_t chunk_bytes, uint8_t *img_base, uint64_t img_origin, const HashOut &h,
-                         hipStream_t s)
+                         uint32_t shift, uint8_t *img_base, uint64_t img_origin, const HashOut &h, hipStream_t s)
 {
     if (count == 0) return hipSuccess;
-    // 2^shift units of kWaves blocks cover a chunk
-    const uint64_t units_per_chunk = (chunk_bytes + kWaves * kBlockBytes - 1) / (kWaves * kBlockBytes);
-    uint32_t shift = 0;
-    while ((1ull << shift) < units_per_chunk) ++shift;
-    if ((count << shift) >> shift != count) return hipErrorInvalidValue;
+    if (shift > kMaxUnitShift || (count << shift) >> shift != count) return hipErrorInvalidValue;
     switch (op * 2 + (hash ? 1 : 0)) {
     case kRestore * 2: return launch_t<kRestore, false>(chunks, first, count, shift, img_base, img_origin, h, s);
     case kRestore * 2 + 1: return launch_t<kRestore, true>(chunks, first, count, shift, img_base, img_origin, h, s);

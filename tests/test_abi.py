@@ -153,3 +153,27 @@ def test_non_contiguous_tensors_refused_by_the_binding():
     with pytest.raises(ValueError, match="non-contiguous"):
         gms.verify(m, blk_hash=torch.zeros(8, 2, dtype=torch.int64)[:, 0], stream=0)
     m.close()
+
+
+def test_launch_groups_split_only_when_idle_units_pay_for_a_launch():
+    """A chunk of at most 8 KiB needs one work unit (two 4 KiB blocks); a 64 KiB chunk needs
+    eight.  Tiny chunks beside large ones get a launch of their own once the idle units they would
+    leave (7 each) reach 16,384; a manifest of similar chunks is a single launch."""
+    big = [64 << 20] * 4
+    assert _host_manifest(big).num_launch_groups == 1
+    assert _host_manifest(big + [100] * 2340).num_launch_groups == 1  # 16,380 idle units
+    assert _host_manifest(big + [100] * 2341).num_launch_groups == 2  # 16,387
+    assert _host_manifest([100] * 200_000).num_launch_groups == 1
+    assert _host_manifest([]).num_launch_groups == 0
+    # a middle class too small to pay for a launch stays in the large chunks' launch
+    m = _host_manifest(big + [100] * 3000 + [20_000] * 10)  # 20,000 B: 5 blocks, 3 units -> 4
+    assert m.num_launch_groups == 2
+    # the weight sets and the KV pool
+    for name, groups in (("tiny", 1), ("llama8b", 1), ("llama70b_tp8", 1), ("moe", 3)):
+        _, ts = synth.weight_set(name)
+        assert _host_manifest([t.nbytes for t in ts]).num_launch_groups == groups, name
+    # the layout does not depend on the grouping
+    sizes = big + [100] * 3000
+    m, m1 = _host_manifest(sizes), _host_manifest(sizes[:4])
+    off, _ = m.layout()
+    assert off[:4] == m1.layout()[0] and m.image_bytes == m1.image_bytes + 3000 * 4096

@@ -35,9 +35,14 @@ def test_traffic_digest_ignores_comments_but_not_code(tmp_path, monkeypatch):
     src = k.read_text()
     k.write_text("// a new comment line\n" + src.replace("namespace gms {", "namespace gms {  /* x */", 1))
     assert bench.kernel_source_digest() == base
-    k.write_text(src.replace("constexpr int kWaves = 2;", "constexpr int kWaves = 4;", 1))
-    assert "constexpr int kWaves = 2;" in src and bench.kernel_source_digest() != base
+    k.write_text(src.replace("constexpr uint32_t kXcds = 8;", "constexpr uint32_t kXcds = 4;", 1))
+    assert "constexpr uint32_t kXcds = 8;" in src and bench.kernel_source_digest() != base
     k.write_text(src)
+    c = tmp_path / bench.CHUNKING[0]
+    cs = c.read_text()
+    c.write_text(cs.replace("constexpr uint64_t kSplitUnits = 16384;", "constexpr uint64_t kSplitUnits = 8192;", 1))
+    assert "constexpr uint64_t kSplitUnits = 16384;" in cs and bench.kernel_source_digest() != base
+    c.write_text(cs)
     h = tmp_path / bench.HEADER
     hs = h.read_text()
     h.write_text(hs.replace("#define GMS_DEFAULT_CHUNK_BYTES (64u * 1024u)", "#define GMS_DEFAULT_CHUNK_BYTES (256u * 1024u)"))

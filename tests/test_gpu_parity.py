@@ -414,3 +414,36 @@ def test_staging_slice_zero_selects_the_default():
     datas = random_datas(sizes, seed=4)
     arena.fill(datas)
     _round_trip(arena, datas, gms.MEM_HOST_PINNED, staging=(0, 3))
+
+
+@pytest.mark.parametrize("kind,staging", [(gms.MEM_DEVICE, None), (gms.MEM_HOST_PINNED, (1 << 20, 2)),
+                                          (gms.MEM_HOST_PINNED, (0, 0))], ids=["device", "ring_1m_x2", "zero_copy"])
+def test_mixed_manifest_takes_several_launch_groups(kind, staging):
+    """Large entries among 40,000 tiny ones (and some mid-sized): the tiny chunks need one work
+    unit where a 64 KiB chunk needs eight, so the library launches them apart; results equal the
+    oracle, slices of the ring holding chunks of several groups included."""
+    need_gpu()
+    rng = np.random.default_rng(99)
+    sizes = [int(v) for v in rng.integers(1, 4097, 40_000)]
+    for i, v in zip(rng.choice(len(sizes), 12, replace=False), [(3 << 20) + 5, 1 << 20, 65536 * 3 + 7, 9000] * 3):
+        sizes[int(i)] = int(v)
+    sizes[::997] = [0] * len(sizes[::997])
+    arena = Arena(sizes, misalign=lambda r: r.integers(0, 16) if r.random() < 0.3 else 0, gap=16, seed=99)
+    datas = random_datas(sizes, seed=99)
+    host = np.full(arena.total, SENTINEL, dtype=np.uint8)
+    for o, d in zip(arena.offsets, datas):
+        host[o:o + d.size] = d
+    arena.buf.copy_(torch.from_numpy(host))
+    m, _ = _round_trip(arena, datas, kind, staging=staging)
+    assert m.num_launch_groups == 2
+    # the host-image path over the same groups (it needs ring slots)
+    m.set_staging(1 << 20, 2)
+    o_img = oracle.pack(datas)
+    arena.poison()
+    cnt = u64_dev(1)
+    gms.restore_from_host(m, o_img, expected=from_u64(oracle.hashes(datas)[0]), mismatch_count=cnt)
+    torch.cuda.synchronize()
+    back, whole = arena.read()
+    assert all(np.array_equal(a, b) for a, b in zip(back, datas)) and arena.outside_untouched(whole)
+    assert to_u64(cnt)[0] == 0
+    m.close()
