@@ -30,8 +30,8 @@ sys.path.insert(0, ROOT)
 
 METRIC = "restore+verify GB/s on 1 GPU; seconds to restore a 16 GB weight shard"
 HBM_PEAK_GBS = 8000.0
-ALL_ROWS = ["main", "snapshot", "plain", "verify", "sequential", "tiny", "h2d", "file", "kv", "kv_vmm", "store", "copy",
-            "cpu", "shards"]
+ALL_ROWS = ["main", "snapshot", "plain", "verify", "sequential", "tiny", "mixed", "h2d", "file", "kv", "kv_vmm", "store",
+            "copy", "cpu", "shards"]
 # What shapes the measured kernel's accesses: the kernel and its launch code, the
 # header's block and default chunk sizes and the chunking in manifest creation.
 KERNEL_SOURCES = ["paper_2609_25451_amd/csrc/gms_kernels.hip", "paper_2609_25451_amd/csrc/gms_internal.h"]
@@ -310,6 +310,9 @@ def main():
             "fused_speedup": t / statistics.median(main_times) if main_times else None}
     if "tiny" in rows:
         result_rows["tiny"] = bench_tiny(torch, gms, synth, timer)
+    if "mixed" in rows:
+        result_rows["mixed"] = bench_mixed(torch, gms, synth, timer, tensors,
+                                           statistics.median(main_times) if main_times else None)
     if "copy" in rows:
         a = torch.empty(4 << 30, dtype=torch.uint8, device="cuda")
         b = torch.empty_like(a)
@@ -548,6 +551,40 @@ def bench_tiny(torch, gms, synth, timer):
     out = {"tensors": len(tensors), "payload_bytes": m.payload_bytes, "restore_verify_us": round(t * 1e6, 1),
            "restore_verify_graph_replay_us": round(tg * 1e6, 1), "snapshot_us": round(ts * 1e6, 1)}
     m.close()
+    return out
+
+
+def bench_mixed(torch, gms, synth, timer, tensors, weights_s=None, n_small=200_000, small_bytes=256):
+    """The llama8b weights plus 200,000 small runtime buffers of 256 bytes (seeded bytes), restored
+    and verified in one call.  A small buffer's chunk needs one work unit where a 64 KiB chunk
+    needs eight; the manifest launches them apart (launch groups), so the buffers should cost what
+    they cost alone.  Reported beside the weights-only step and the buffers alone."""
+    small = torch.empty(n_small * 512, dtype=torch.uint8, device="cuda")
+    synth.dev_fill_bf16(small.data_ptr(), small.numel() // 2, 4242, 0)
+    bufs = [(small.data_ptr() + i * 512, small_bytes) for i in range(n_small)]
+
+    def one(entries):
+        m = gms.Manifest(entries, device=0)
+        img = torch.empty(m.image_bytes, dtype=torch.uint8, device="cuda")
+        exp = torch.zeros(m.num_blocks, dtype=torch.int64, device="cuda")
+        gms.snapshot(m, img, m.image_bytes, blk_hash=exp)
+        cnt = torch.zeros(1, dtype=torch.int64, device="cuda")
+        t = settled(timer, lambda: gms.restore(m, img, m.image_bytes, expected=exp, mismatch_count=cnt))
+        assert int(cnt.item()) == 0
+        out = (t, m.num_launch_groups, m.num_chunks)
+        m.close()
+        del img, exp
+        return out
+
+    t_mixed, groups, chunks = one(list(tensors) + bufs)
+    t_small, _, _ = one(bufs)
+    del small
+    torch.cuda.empty_cache()
+    out = {"entries": len(tensors) + n_small, "small_buffers": n_small, "small_bytes": small_bytes, "chunks": chunks,
+           "launch_groups": groups, "restore_verify_s": t_mixed, "small_buffers_alone_s": t_small}
+    if weights_s:
+        out["weights_only_s"] = weights_s
+        out["added_by_small_buffers_s"] = t_mixed - weights_s
     return out
 
 
