@@ -278,16 +278,20 @@ constexpr uint64_t kMaxGrid = 1ull << 30;  // a multiple of kXcds
 // Dynamic LDS per workgroup: restore and snapshot ask for a sixth of a CU's
 // 160 KiB so that six 2-wave workgroups are resident per CU; verify
 // (read-only, heavier on VALU per byte) only needs the wave partials and runs
-// at full occupancy.
+// at full occupancy.  So do launches of one unit per chunk (chunks of at most
+// two blocks): each workgroup then moves at most 8 KiB behind two dependent
+// loads, and more of them in flight hide that latency (200,000 one-block
+// entries: 0.52 ms at six per CU, 0.24 ms at full occupancy).
 constexpr size_t kLdsCopy = 26 * 1024;
-constexpr size_t kLdsVerify = kWaves * sizeof(uint64_t);
+constexpr size_t kLdsSmall = kWaves * sizeof(uint64_t);
 
 template <int OP, bool HASH>
 hipError_t launch_t(const Chunk *chunks, uint64_t first, uint64_t count, uint32_t unit_shift, uint8_t *img_base,
                     uint64_t img_origin, const HashOut &h, hipStream_t s)
 {
-    constexpr size_t lds = OP == kVerify ? kLdsVerify : kLdsCopy;
-    static_assert(lds <= 64 * 1024, "above 64 KiB the launch would have to opt in per device");
+    constexpr size_t lds_stream = OP == kVerify ? kLdsSmall : kLdsCopy;
+    static_assert(lds_stream <= 64 * 1024, "above 64 KiB the launch would have to opt in per device");
+    const size_t lds = unit_shift == 0 ? kLdsSmall : lds_stream;
     const uint64_t units = count << unit_shift;
     const uint64_t grid = ((units < kMaxGrid ? units : kMaxGrid) + kXcds - 1) / kXcds * kXcds;
     hipLaunchKernelGGL((k_stream<OP, HASH>), dim3((uint32_t)grid), dim3(kUnitThreads), lds, s, chunks + first, count,
