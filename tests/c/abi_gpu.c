@@ -2,15 +2,18 @@
  * C99 client of include/gms.h on the GPU, with no Python or torch: device
  * memory from hipMalloc, streams as plain HIP handles.  Snapshot, restore and
  * verify results are compared with the C oracle (linked beside the library,
- * sharing nothing with it) on the same host bytes, for device images and for a
- * pageable host image; the model-state store is driven through one commit and
- * one verified read-only lease.  Exits non-zero
+ * sharing nothing with it) on the same host bytes, for device images, a pinned
+ * image through a small staging ring, an image file and a pageable host image;
+ * the model-state store is driven through one commit and one verified
+ * read-only lease.  Exits non-zero
  * on the first failed check, printing it.
  */
+#define _POSIX_C_SOURCE 200809L /* mkstemp, close, unlink */
 #include <stdint.h>
 #include <stdio.h>
 #include <stdlib.h>
 #include <string.h>
+#include <unistd.h>
 
 #include <hip/hip_runtime_api.h>
 
@@ -126,6 +129,40 @@ int main(void)
     CHECK(gms_restore_from_host(m, h_img, ib - 1, 0, NULL, NULL, NULL, NULL, NULL, 0, s) == GMS_ERR_SIZE);
     CHECK(gms_snapshot_to_host(m, d_img, ib, 0, NULL, NULL, s) == GMS_ERR_INVALID); /* device memory */
     free(h_img);
+
+    /* pinned host image through a staging ring of 64 KiB slices (many slices, the ring wraps) */
+    uint8_t *p_img = NULL;
+    CHECK(hipHostMalloc((void **)&p_img, ib, 0) == hipSuccess);
+    memcpy(p_img, o_img, ib);
+    CHECK(gms_manifest_set_staging(m, 64 * 1024, 2) == GMS_OK);
+    for (int i = 0; i < N; ++i) CHECK(hipMemset(dev[i] + mis[i], 0x44, sizes[i]) == hipSuccess);
+    CHECK(gms_restore(m, p_img, ib, GMS_MEM_HOST_PINNED, d_exp, NULL, NULL, d_cnt, NULL, 0, s) == GMS_OK);
+    CHECK(hipStreamSynchronize(s) == hipSuccess);
+    CHECK(hipMemcpy(&cnt, d_cnt, 8, hipMemcpyDeviceToHost) == hipSuccess && cnt == 0);
+    for (int i = 0; i < N; ++i) {
+        CHECK(hipMemcpy(back[i], dev[i] + mis[i], sizes[i], hipMemcpyDeviceToHost) == hipSuccess);
+        CHECK(memcmp(back[i], host[i], sizes[i]) == 0);
+    }
+    memset(p_img, 0, ib);
+    CHECK(gms_snapshot(m, p_img, ib, GMS_MEM_HOST_PINNED, NULL, NULL, s) == GMS_OK);
+    CHECK(hipStreamSynchronize(s) == hipSuccess && memcmp(p_img, o_img, ib) == 0);
+    CHECK(hipHostFree(p_img) == hipSuccess);
+
+    /* an image file, buffered I/O, 3 workers */
+    char path[] = "/tmp/gms_abi_gpu_XXXXXX";
+    int fd = mkstemp(path);
+    CHECK(fd >= 0);
+    close(fd);
+    CHECK(gms_snapshot_to_file(m, path, 0, 3, NULL, NULL, s) == GMS_OK);
+    for (int i = 0; i < N; ++i) CHECK(hipMemset(dev[i] + mis[i], 0x55, sizes[i]) == hipSuccess);
+    CHECK(gms_restore_from_file(m, path, 0, 0, 3, d_exp, NULL, NULL, d_cnt, NULL, 0, s) == GMS_OK);
+    CHECK(hipStreamSynchronize(s) == hipSuccess);
+    CHECK(hipMemcpy(&cnt, d_cnt, 8, hipMemcpyDeviceToHost) == hipSuccess && cnt == 0);
+    for (int i = 0; i < N; ++i) {
+        CHECK(hipMemcpy(back[i], dev[i] + mis[i], sizes[i], hipMemcpyDeviceToHost) == hipSuccess);
+        CHECK(memcmp(back[i], host[i], sizes[i]) == 0);
+    }
+    unlink(path);
 
     /* the model-state store: populate, commit, verified read-only lease */
     gms_store *st = NULL;
