@@ -364,6 +364,8 @@ int run_ring(gms_manifest *m, int op, const HashOut &h, uint8_t *host_image, hip
         GMS_TRY(hipStreamWaitEvent(m->copy_stream, m->ev_done, 0));
         GMS_TRY(hipStreamWaitEvent(s, m->ev_done, 0));
     }
+    gms::RingFence fence(m, s);
+    fence.armed = true;
     for (uint64_t sl = 0; sl < nslices; ++sl) {
         const uint32_t slot = (uint32_t)(sl % k);
         uint8_t *dev = m->d_ring + (uint64_t)slot * slice;
@@ -383,9 +385,7 @@ int run_ring(gms_manifest *m, int op, const HashOut &h, uint8_t *host_image, hip
         GMS_TRY(hipEventRecord(m->ev_free[slot], consumer));
     }
     // the call ends on the caller's stream once the last slot is consumed
-    GMS_TRY(hipEventRecord(m->ev_done, consumer));
-    if (to_host) GMS_TRY(hipStreamWaitEvent(s, m->ev_done, 0));
-    m->done_recorded = true;
+    GMS_TRY(fence.close());
 #undef GMS_TRY
     return GMS_OK;
 }

@@ -92,6 +92,34 @@ struct gms_manifest {
 
 namespace gms {
 
+// Ends a ring call: joins the caller's stream and the copy stream and records
+// ev_done after both, so the next ring call on the manifest, from any stream,
+// waits until this one no longer uses a slot.  Once armed, a call that fails
+// half-way still fences what it had enqueued (best effort, in the destructor).
+struct RingFence {
+    gms_manifest *m;
+    hipStream_t s;
+    bool armed = false;
+    RingFence(gms_manifest *m_, hipStream_t s_) : m(m_), s(s_) {}
+    // success path: the call's work then completes on `s`
+    hipError_t close()
+    {
+        armed = false;
+        hipError_t e;
+        if ((e = hipEventRecord(m->ev_entry, s)) != hipSuccess) return e;
+        if ((e = hipStreamWaitEvent(m->copy_stream, m->ev_entry, 0)) != hipSuccess) return e;
+        if ((e = hipEventRecord(m->ev_done, m->copy_stream)) != hipSuccess) return e;
+        m->done_recorded = true;
+        return hipStreamWaitEvent(s, m->ev_done, 0);
+    }
+    ~RingFence()
+    {
+        if (armed && close() != hipSuccess) (void)hipGetLastError();
+    }
+    RingFence(const RingFence &) = delete;
+    RingFence &operator=(const RingFence &) = delete;
+};
+
 // pool internals used by the model-state store
 int pool_reset(gms_pool *p);
 int pool_set_access_all(gms_pool *p, bool read_only);

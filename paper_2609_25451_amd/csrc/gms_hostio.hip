@@ -340,6 +340,8 @@ int restore_pipeline(gms_manifest *m, const HostImage &src, const HashOut &h, un
     const uint32_t k = m->ring_slots, hk = m->host_slots;
     GMS_TRY(hipEventRecord(m->ev_entry, s));
     GMS_TRY(hipStreamWaitEvent(m->copy_stream, m->ev_entry, 0));
+    gms::RingFence fence(m, s);
+    fence.armed = true;
 
     PiecePool pool(slice, m->image_bytes, piece);
     Workers w(pool, src, false, m->h_ring, hk, m->ev_host, (unsigned)std::min<uint64_t>(threads, pool.npieces));
@@ -364,8 +366,7 @@ int restore_pipeline(gms_manifest *m, const HostImage &src, const HashOut &h, un
         pool.set_enqueued(sl + 1);
     }
     if ((rc = finish(pool, w, rc, src, false)) != GMS_OK) return rc;
-    GMS_TRY(hipEventRecord(m->ev_done, s));
-    m->done_recorded = true;
+    GMS_TRY(fence.close());
     return GMS_OK;
 }
 
@@ -408,6 +409,8 @@ int snapshot_pipeline(gms_manifest *m, const HostImage &dst, const HashOut &h, u
         return GMS_OK;
     };
 
+    gms::RingFence fence(m, s);
+    fence.armed = true;
     PiecePool pool(slice, m->image_bytes, piece);
     Workers w(pool, dst, true, m->h_ring, hk, m->ev_host, (unsigned)std::min<uint64_t>(threads, pool.npieces));
     const uint64_t first = std::min<uint64_t>(hk, pool.nslices);
@@ -418,9 +421,7 @@ int snapshot_pipeline(gms_manifest *m, const HostImage &dst, const HashOut &h, u
         if ((rc = enqueue(sl + hk)) == GMS_OK) pool.set_enqueued(sl + hk + 1);
     }
     if ((rc = finish(pool, w, rc, dst, true)) != GMS_OK) return rc;
-    // every slice has been through its host slot, so the device work is done
-    GMS_TRY(hipEventRecord(m->ev_done, via_device ? m->copy_stream : s));
-    m->done_recorded = true;
+    GMS_TRY(fence.close());
     return GMS_OK;
 }
 
