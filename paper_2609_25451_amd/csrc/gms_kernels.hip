@@ -1,7 +1,9 @@
 // Gather / scatter / verify kernels for gfx950.
 //
 // The unit of work is two 4 KiB blocks of one chunk of the manifest's work
-// list, taken by one 2-wave workgroup: each wave moves and hashes one block.
+// list, taken by one 2-wave workgroup: each wave moves and hashes one block
+// (k_stream).  Launches of chunks of at most two blocks give each wave a whole
+// chunk instead (k_pair).
 // For a block a lane moves four 16-byte segments at byte offsets
 // k*1024 + lane*16 (k = 0..3), so every load and store instruction of the
 // wave covers 1 KiB contiguously.  Small, short-lived workgroups let the
@@ -170,13 +172,80 @@ __device__ __forceinline__ uint32_t fast_blocks(const Chunk &c)
     return (c.addr & 15) == 0 ? c.len / kBlockBytes : 0;
 }
 
+// Block b of chunk c, by one wave.  A full, aligned block is loaded with
+// 16-byte non-temporal loads, stored and hashed from the same registers; its
+// expected hash is loaded branch-free (a harmless address when not checking)
+// just before its data and folded into the wave reduction.  The ragged last
+// block of an entry and every block of an unaligned entry take byte-granular
+// code.  Returns the block hash (in lane 0), or 0 past the chunk's end.
+template <int OP, bool HASH>
+__device__ __forceinline__ uint64_t move_block(const Chunk &c, uint32_t b, gbyte *img_base, uint64_t img_origin,
+                                               const HashOut &h, uint32_t lane, bool check,
+                                               const uint64_t *exp_dummy)
+{
+    const uint32_t nblk = (c.len + kBlockBytes - 1) / kBlockBytes;
+    const uint32_t nfull = fast_blocks(c);
+    const bool aligned = (c.addr & 15) == 0;
+    gbyte *const img = img_base + (c.img - img_origin) + (size_t)b * kBlockBytes + lane * 16;
+    gbyte *const ent = (gbyte *)c.addr + (size_t)b * kBlockBytes + lane * 16;
+    const uint64_t jg0 = (c.off >> 3) * kG + (uint64_t)b * kBlockStrideG + 2ull * lane * kG;
+    const uint64_t gblk = (c.img >> 12) + b;
+    uint64_t tacc = 0;
+
+    if (b < nfull) {  // full aligned block
+        uint64_t want = 0;
+        if (HASH) want = *(check ? h.expected + gblk : exp_dummy);
+        u32x4 v[4];
+        load_block(v, OP == kRestore ? img : ent);
+        if (OP != kVerify) store_block(v, OP == kRestore ? ent : img);
+        if (HASH) {
+            uint64_t hl = 0;
+#pragma unroll
+            for (int k = 0; k < 4; ++k) hl ^= seg_hash(v[k], jg0 + (uint64_t)k * kSegStrideG);
+            tacc = finish_block(hl, gblk, h, lane, check, want);
+        }
+    } else if (b < nblk) {  // ragged last block, or a block of an unaligned entry
+        const uint32_t boff = b * kBlockBytes;
+        uint64_t hl = 0;
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+            const uint32_t p = boff + k * 1024 + lane * 16;  // chunk-relative
+            const uint32_t valid = p >= c.len ? 0u : min(16u, c.len - p);
+            u32x4 v;
+            if (OP == kRestore) {
+                v = keep_bytes(*(const gvec *)(img + k * 1024), valid);
+                store_part(ent + k * 1024, v, valid, aligned);
+            } else {
+                v = load_part(ent + k * 1024, valid, aligned);
+                if (OP == kSnapshot) *(gvec *)(img + k * 1024) = v;
+            }
+            if (HASH) {
+                const uint64_t jg = jg0 + (uint64_t)k * kSegStrideG;
+                uint64_t w0 = (uint64_t)v.x | ((uint64_t)v.y << 32);
+                uint64_t w1 = (uint64_t)v.z | ((uint64_t)v.w << 32);
+                if (valid > 0) hl ^= mix64(w0 ^ jg);
+                if (valid > 8) hl ^= mix64(w1 ^ (jg + kG));
+            }
+        }
+        if (HASH) tacc = finish_block(hl, gblk, h, lane, check, check ? h.expected[gblk] : 0);
+    }
+    return tacc;
+}
+
+// XCD-aware order: the dispatcher hands workgroup IDs to the 8 XCDs round
+// robin, so within each grid-sized round, XCD x takes the x-th contiguous
+// eighth of the units and every XCD streams its own contiguous region of the
+// image and of the entries.
+__device__ __forceinline__ uint64_t xcd_slot()
+{
+    const uint64_t per_xcd = gridDim.x / kXcds;  // the grid is a multiple of kXcds
+    return (blockIdx.x % kXcds) * per_xcd + blockIdx.x / kXcds;
+}
+
 // Unit u is blocks [(u mod 2^shift) * kWaves, +kWaves) of chunk u >> shift
-// (2^shift units cover the manifest's longest chunk); wave w of the workgroup
-// takes the unit's block w.  A full, aligned block is loaded with 16-byte
-// non-temporal loads, stored and hashed from the same registers; its expected
-// hash is loaded branch-free (a harmless address when not checking) just
-// before its data and folded into the wave reduction.  The ragged last block
-// of an entry and every block of an unaligned entry take byte-granular code.
+// (2^shift units cover the launch's longest chunk); wave w of the workgroup
+// takes the unit's block w.  Tensor hashes combine the two waves' block
+// hashes in LDS and take one atomic XOR per unit.
 template <int OP, bool HASH>
 __global__ void __launch_bounds__(kUnitThreads)
 k_stream(const Chunk *__restrict__ chunks, uint64_t count, uint32_t unit_shift, gbyte *__restrict__ img_base,
@@ -185,69 +254,17 @@ k_stream(const Chunk *__restrict__ chunks, uint64_t count, uint32_t unit_shift, 
     extern __shared__ uint64_t wave_part[];  // kWaves words used
     const uint32_t lane = threadIdx.x & 63;
     const uint32_t wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);  // wave-uniform
-    const uint64_t lane_g = 2ull * lane * kG;  // j*G offset of the lane's first word in a block
     const bool check = HASH && h.expected != nullptr;
     const uint64_t *const exp_dummy = (const uint64_t *)chunks;  // any readable word
     const uint64_t units = count << unit_shift;
     const uint32_t unit_mask = (1u << unit_shift) - 1;
-
-    // XCD-aware order: the dispatcher hands workgroup IDs to the 8 XCDs round
-    // robin, so within each grid-sized round, XCD x takes the x-th contiguous
-    // eighth of the units and every XCD streams its own contiguous region of
-    // the image and of the entries.
-    const uint64_t per_xcd = gridDim.x / kXcds;  // the grid is a multiple of kXcds
-    const uint64_t slot_in_round = (blockIdx.x % kXcds) * per_xcd + blockIdx.x / kXcds;
+    const uint64_t slot_in_round = xcd_slot();
     for (uint64_t round = 0; round < units; round += gridDim.x) {
         const uint64_t u = round + slot_in_round;
         if (u >= units) break;  // uniform across the workgroup
         const Chunk c = chunks[u >> unit_shift];
         const uint32_t b = ((uint32_t)u & unit_mask) * kWaves + wave;  // the wave's block of the chunk
-        const uint32_t nblk = (c.len + kBlockBytes - 1) / kBlockBytes;
-        const uint32_t nfull = fast_blocks(c);
-        const bool aligned = (c.addr & 15) == 0;
-        gbyte *const img = img_base + (c.img - img_origin) + (size_t)b * kBlockBytes + lane * 16;
-        gbyte *const ent = (gbyte *)c.addr + (size_t)b * kBlockBytes + lane * 16;
-        const uint64_t jg0 = (c.off >> 3) * kG + (uint64_t)b * kBlockStrideG + lane_g;
-        const uint64_t gblk = (c.img >> 12) + b;
-        uint64_t tacc = 0;
-
-        if (b < nfull) {  // full aligned block
-            uint64_t want = 0;
-            if (HASH) want = *(check ? h.expected + gblk : exp_dummy);
-            u32x4 v[4];
-            load_block(v, OP == kRestore ? img : ent);
-            if (OP != kVerify) store_block(v, OP == kRestore ? ent : img);
-            if (HASH) {
-                uint64_t hl = 0;
-#pragma unroll
-                for (int k = 0; k < 4; ++k) hl ^= seg_hash(v[k], jg0 + (uint64_t)k * kSegStrideG);
-                tacc = finish_block(hl, gblk, h, lane, check, want);
-            }
-        } else if (b < nblk) {  // ragged last block, or a block of an unaligned entry
-            const uint32_t boff = b * kBlockBytes;
-            uint64_t hl = 0;
-#pragma unroll
-            for (int k = 0; k < 4; ++k) {
-                const uint32_t p = boff + k * 1024 + lane * 16;  // chunk-relative
-                const uint32_t valid = p >= c.len ? 0u : min(16u, c.len - p);
-                u32x4 v;
-                if (OP == kRestore) {
-                    v = keep_bytes(*(const gvec *)(img + k * 1024), valid);
-                    store_part(ent + k * 1024, v, valid, aligned);
-                } else {
-                    v = load_part(ent + k * 1024, valid, aligned);
-                    if (OP == kSnapshot) *(gvec *)(img + k * 1024) = v;
-                }
-                if (HASH) {
-                    const uint64_t jg = jg0 + (uint64_t)k * kSegStrideG;
-                    uint64_t w0 = (uint64_t)v.x | ((uint64_t)v.y << 32);
-                    uint64_t w1 = (uint64_t)v.z | ((uint64_t)v.w << 32);
-                    if (valid > 0) hl ^= mix64(w0 ^ jg);
-                    if (valid > 8) hl ^= mix64(w1 ^ (jg + kG));
-                }
-            }
-            if (HASH) tacc = finish_block(hl, gblk, h, lane, check, check ? h.expected[gblk] : 0);
-        }
+        const uint64_t tacc = move_block<OP, HASH>(c, b, img_base, img_origin, h, lane, check, exp_dummy);
 
         // ---- tensor hash: XOR of the workgroup's block hashes, one atomic per unit
         if (HASH && h.ten) {
@@ -261,6 +278,36 @@ k_stream(const Chunk *__restrict__ chunks, uint64_t count, uint32_t unit_shift, 
             }
             __syncthreads();
         }
+    }
+}
+
+// Launches of one unit per chunk (chunks of at most kWaves blocks): a
+// one-block chunk would leave the unit's second wave idle, so instead wave w
+// of unit u takes all of chunk 2u + w, and each wave adds its chunk's hash to
+// the tensor hash itself.  No barrier: a wave past the last chunk just skips.
+template <int OP, bool HASH>
+__global__ void __launch_bounds__(kUnitThreads)
+k_pair(const Chunk *__restrict__ chunks, uint64_t count, gbyte *__restrict__ img_base, uint64_t img_origin,
+       HashOut h)
+{
+    const uint32_t lane = threadIdx.x & 63;
+    const uint32_t wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);  // wave-uniform
+    const bool check = HASH && h.expected != nullptr;
+    const uint64_t *const exp_dummy = (const uint64_t *)chunks;
+    const uint64_t units = (count + kWaves - 1) / kWaves;
+    const uint64_t slot_in_round = xcd_slot();
+    for (uint64_t round = 0; round < units; round += gridDim.x) {
+        const uint64_t u = round + slot_in_round;
+        if (u >= units) break;
+        const uint64_t ci = u * kWaves + wave;
+        if (ci >= count) continue;  // wave-uniform
+        const Chunk c = chunks[ci];
+        const uint32_t nblk = (c.len + kBlockBytes - 1) / kBlockBytes;  // at most kWaves
+        uint64_t tacc = 0;
+        for (uint32_t b = 0; b < nblk; ++b)
+            tacc ^= move_block<OP, HASH>(c, b, img_base, img_origin, h, lane, check, exp_dummy);
+        if (HASH && h.ten && lane == 0 && tacc)
+            atomicXor((unsigned long long *)(h.ten + c.entry), (unsigned long long)tacc);
     }
 }
 
@@ -279,23 +326,28 @@ constexpr uint64_t kMaxGrid = 1ull << 30;  // a multiple of kXcds
 // 160 KiB so that six 2-wave workgroups are resident per CU; verify
 // (read-only, heavier on VALU per byte) only needs the wave partials and runs
 // at full occupancy.  So do launches of one unit per chunk (chunks of at most
-// two blocks): each workgroup then moves at most 8 KiB behind two dependent
+// two blocks, k_pair): each wave then moves at most 8 KiB behind two dependent
 // loads, and more of them in flight hide that latency (200,000 one-block
-// entries: 0.52 ms at six per CU, 0.24 ms at full occupancy).
+// entries: 0.52 ms at six workgroups per CU, 0.24 ms at full occupancy).
 constexpr size_t kLdsCopy = 26 * 1024;
-constexpr size_t kLdsSmall = kWaves * sizeof(uint64_t);
+constexpr size_t kLdsVerify = kWaves * sizeof(uint64_t);
+
+uint64_t grid_for(uint64_t units) { return ((units < kMaxGrid ? units : kMaxGrid) + kXcds - 1) / kXcds * kXcds; }
 
 template <int OP, bool HASH>
 hipError_t launch_t(const Chunk *chunks, uint64_t first, uint64_t count, uint32_t unit_shift, uint8_t *img_base,
                     uint64_t img_origin, const HashOut &h, hipStream_t s)
 {
-    constexpr size_t lds_stream = OP == kVerify ? kLdsSmall : kLdsCopy;
-    static_assert(lds_stream <= 64 * 1024, "above 64 KiB the launch would have to opt in per device");
-    const size_t lds = unit_shift == 0 ? kLdsSmall : lds_stream;
-    const uint64_t units = count << unit_shift;
-    const uint64_t grid = ((units < kMaxGrid ? units : kMaxGrid) + kXcds - 1) / kXcds * kXcds;
-    hipLaunchKernelGGL((k_stream<OP, HASH>), dim3((uint32_t)grid), dim3(kUnitThreads), lds, s, chunks + first, count,
-                       unit_shift, (gbyte *)img_base, img_origin, h);
+    if (unit_shift == 0) {
+        const uint64_t grid = grid_for((count + kWaves - 1) / kWaves);
+        hipLaunchKernelGGL((k_pair<OP, HASH>), dim3((uint32_t)grid), dim3(kUnitThreads), 0, s, chunks + first, count,
+                           (gbyte *)img_base, img_origin, h);
+        return hipGetLastError();
+    }
+    constexpr size_t lds = OP == kVerify ? kLdsVerify : kLdsCopy;
+    static_assert(lds <= 64 * 1024, "above 64 KiB the launch would have to opt in per device");
+    hipLaunchKernelGGL((k_stream<OP, HASH>), dim3((uint32_t)grid_for(count << unit_shift)), dim3(kUnitThreads), lds,
+                       s, chunks + first, count, unit_shift, (gbyte *)img_base, img_origin, h);
     return hipGetLastError();
 }
 
