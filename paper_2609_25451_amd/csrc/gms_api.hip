@@ -145,26 +145,36 @@ void plan_launch_groups(gms_manifest *m)
     // from the largest down, a class gets a launch of its own (shared with the
     // smaller classes after it) once the idle units it would leave reach
     // kSplitUnits; a manifest of similar chunks stays one launch.
+    const uint64_t n = m->chunks.size();
+    std::vector<uint8_t> cls(n);
     uint64_t count[kMaxUnitShift + 1] = {};
-    for (const Chunk &c : m->chunks) ++count[unit_class(c.len)];
+    for (uint64_t i = 0; i < n; ++i) ++count[cls[i] = (uint8_t)unit_class(m->chunks[i].len)];
     uint32_t group_of[kMaxUnitShift + 1] = {};
     int top = kMaxUnitShift;
     while (top > 0 && count[top] == 0) --top;
     uint32_t g = (uint32_t)top;
+    std::vector<uint32_t> shifts;  // group shifts, largest first
     for (int s = top; s >= 0; --s) {
         if (count[s] && (uint32_t)s < g && count[s] * ((1ull << g) - (1ull << s)) >= kSplitUnits) g = (uint32_t)s;
         group_of[s] = g;
+        if (count[s] && (shifts.empty() || shifts.back() != g)) shifts.push_back(g);
     }
-    // chunks by group (larger shift first), in image order within a group
-    std::stable_sort(m->chunks.begin(), m->chunks.end(), [&](const Chunk &a, const Chunk &b) {
-        return group_of[unit_class(a.len)] > group_of[unit_class(b.len)];
-    });
     m->groups.clear();
-    for (uint64_t i = 0; i < m->chunks.size(); ++i) {
-        const uint32_t sh = group_of[unit_class(m->chunks[i].len)];
-        if (m->groups.empty() || m->groups.back().shift != sh) m->groups.push_back(LaunchGroup{i, 0, sh});
-        ++m->groups.back().count;
+    if (shifts.size() == 1) {
+        m->groups.push_back(LaunchGroup{0, n, shifts[0]});
+        return;
     }
+    // chunks by group, larger shift first, in image order within a group
+    std::vector<Chunk> sorted;
+    sorted.reserve(n);
+    for (uint32_t sh : shifts) {
+        LaunchGroup lg{sorted.size(), 0, sh};
+        for (uint64_t i = 0; i < n; ++i)
+            if (group_of[cls[i]] == sh) sorted.push_back(m->chunks[i]);
+        lg.count = sorted.size() - lg.first;
+        m->groups.push_back(lg);
+    }
+    m->chunks.swap(sorted);
 }
 
 hipError_t launch_all(const gms_manifest *m, int op, const HashOut &h, uint8_t *img_base, hipStream_t s)
@@ -515,6 +525,9 @@ int gms_manifest_create(const gms_entry *entries, uint64_t n, int device, uint64
         m->n = n;
         m->chunk_bytes = chunk_bytes;
         m->img_off.resize(n);
+        uint64_t most = 0;  // an entry splits into at most nbytes / chunk_bytes + 2 chunks
+        for (uint64_t i = 0; i < n; ++i) most += entries[i].nbytes ? entries[i].nbytes / chunk_bytes + 2 : 0;
+        m->chunks.reserve(most);
         uint64_t off = 0;
         for (uint64_t i = 0; i < n; ++i) {
             const uint64_t nb = entries[i].nbytes;
