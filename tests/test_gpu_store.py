@@ -245,3 +245,73 @@ def test_cold_repopulation_from_file(tmp_path):
     assert s.state() == ("COMMITTED", 0, False)
     m.close()
     s.close()
+
+
+def test_recovery_sequence_weights_resident_kv_from_host():
+    """The recovery data path at small scale.  The weights stay resident in the committed store;
+    the live KV units were saved with their hashes to pageable host memory and the engine's KV
+    pages released.  The replacement attaches to the weights after re-hashing them, remaps the
+    KV pages at the same addresses and restores the live units from the host image with fused
+    verification: live units equal the oracle's bytes, dead units keep what the fresh pages
+    held, and a damaged host image is flagged at exactly its block."""
+    need_gpu()
+    s = gms.Store(va_bytes=1 << 30, slab_bytes=SLAB)
+    w = s.connect_rw()
+    entries, datas = _populate(w, seed=34)
+    o_blk, _ = oracle.hashes(datas)
+    w.commit(entries, expected=from_u64(o_blk))
+    engine = s.connect_ro()
+
+    layers, blocks, unit = 4, 64, 64 << 10
+    slab = blocks * unit
+    pool = gms.Pool(va_bytes=layers * slab + (64 << 20), slab_bytes=slab)
+    kv = [pool.alloc(slab) for _ in range(layers)]
+    kv_data = []
+    for l, a in enumerate(kv):
+        synth.dev_fill_bf16(a, slab // 2, 35, l)
+        kv_data.append(synth.bf16_bits(slab // 2, 35, l).view(np.uint8))
+    live = np.sort(np.random.default_rng(36).choice(blocks, blocks // 2, replace=False))
+    ents = [(kv[l] + int(b) * unit, unit) for l in range(layers) for b in live]
+    want = [kv_data[l][int(b) * unit:(int(b) + 1) * unit] for l in range(layers) for b in live]
+    km = gms.Manifest(ents)
+    host = np.zeros(km.image_bytes, dtype=np.uint8)
+    kv_exp = u64_dev(km.num_blocks)
+    gms.snapshot_to_host(km, host, blk_hash=kv_exp)
+    assert np.array_equal(host, oracle.pack(want))
+    o_kv = oracle.hashes(want)[0]
+    assert np.array_equal(to_u64(kv_exp, km.num_blocks), o_kv)
+
+    # the failure: the engine's lease ends, its KV pages are released
+    engine.close()
+    for a in kv:
+        pool.release(a, slab)
+
+    # recovery
+    r = s.connect_ro(verify=True)
+    assert s.state() == ("RO", 1, False)
+    for a in kv:
+        pool.remap(a, slab)
+        memset(a, 0x5A, slab)  # what the fresh pages hold before the restore
+    cnt = u64_dev(1)
+    gms.restore_from_host(km, host, expected=from_u64(o_kv), mismatch_count=cnt)
+    torch.cuda.synchronize()
+    assert to_u64(cnt)[0] == 0
+    dead = np.setdiff1d(np.arange(blocks), live)
+    for l, a in enumerate(kv):
+        got = d2h(a, slab).reshape(blocks, unit)
+        for b in live:
+            assert np.array_equal(got[b], kv_data[l][int(b) * unit:(int(b) + 1) * unit]), (l, b)
+        assert (got[dead] == 0x5A).all(), f"layer {l}: a dead unit was written"
+
+    # a damaged host image: exactly its block is flagged
+    off, base = km.layout()
+    e = len(ents) // 3
+    host[off[e] + 5 * 4096 + 77] ^= 0x08
+    lst = u64_dev(4)
+    gms.restore_from_host(km, host, expected=from_u64(o_kv), mismatch_count=cnt, mismatch_list=lst, mismatch_cap=4)
+    torch.cuda.synchronize()
+    assert to_u64(cnt)[0] == 1 and int(to_u64(lst, 1)[0]) == int(base[e]) + 5
+    r.close()
+    km.close()
+    pool.close()
+    s.close()
