@@ -113,11 +113,18 @@ def test_data_plane_refused_on_host_only_manifest():
     with pytest.raises(gms.GmsError) as e:
         m.set_staging(1 << 20, 2)
     assert e.value.status == gms.GMS_ERR_STATE
+    host = np.zeros(m.image_bytes, dtype=np.uint8)
     for call in (lambda: gms.restore_from_file(m, "/nonexistent"),
-                 lambda: gms.snapshot_to_file(m, "/nonexistent")):
+                 lambda: gms.snapshot_to_file(m, "/nonexistent"),
+                 lambda: gms.restore_from_host(m, host, stream=0),
+                 lambda: gms.snapshot_to_host(m, host, stream=0)):
         with pytest.raises(gms.GmsError) as e:
             call()
         assert e.value.status == gms.GMS_ERR_STATE
+    with pytest.raises(ValueError, match="non-contiguous"):  # refused by the binding before the call
+        gms.snapshot_to_host(m, np.zeros((2, m.image_bytes), np.uint8)[:, ::2], stream=0)
+    with pytest.raises(ValueError, match="image_bytes"):
+        gms.restore_from_host(m, 1 << 30, stream=0)
 
 
 def test_null_arguments():
