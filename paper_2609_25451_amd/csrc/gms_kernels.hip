@@ -14,7 +14,8 @@
 // the registers that were just moved: each lane mixes its eight 8-byte words,
 // the wave XOR-reduces its 64 partials with DPP row operations plus four lane
 // reads, and lane 0 stores / compares the block hash.  Tensor hashes combine
-// the two waves' XORs in LDS and take one 64-bit atomic XOR per unit.
+// the two waves' XORs in LDS and take one 64-bit atomic XOR per unit (k_pair:
+// one per chunk, from its wave).
 //
 // Bandwidth path: no MFMA; 16-byte non-temporal loads and stores for the
 // streaming side; byte-granular code only for unaligned entries and the ragged
