@@ -339,7 +339,8 @@ using gms::check_common;
 using gms::check_outputs;
 using gms::ensure_ring;
 
-// Device-resident image, or zero-copy access to a pinned one: one launch.
+// Device-resident image, or zero-copy access to a pinned one: one launch per
+// launch group.
 int run_direct(const gms_manifest *m, int op, uint8_t *image, const HashOut &h, hipStream_t s)
 {
     hipError_t e = gms::launch_all(m, op, h, image, s);
@@ -400,8 +401,8 @@ int run_ring(gms_manifest *m, int op, const HashOut &h, uint8_t *host_image, hip
     return GMS_OK;
 }
 
-// Device images take one launch.  A pinned image goes through the staging
-// ring, except with no ring slots, and except a snapshot with slices below
+// Device images take one launch per launch group.  A pinned image goes through
+// the staging ring, except with no ring slots, and except a snapshot with slices below
 // gms::kRingSnapshotMinSlice: those access the image zero-copy over the host link.
 int run_op(const gms_manifest *cm, int op, void *image, int kind, const HashOut &h, void *stream)
 {
