@@ -347,10 +347,10 @@ int run_direct(const gms_manifest *m, int op, uint8_t *image, const HashOut &h, 
     return e == hipSuccess ? GMS_OK : fail_hip(e, "kernel launch");
 }
 
-// A pinned image through the staging ring.  Restore: DMA slice -> device slot
-// on the copy stream, then the scatter kernel reads the slot on the caller's
-// stream.  Snapshot: the gather kernel fills the slot on the caller's stream,
-// then the copy stream DMAs it to the host image.  The slot's producer reuses
+// A pinned image through the staging ring.  Restore: the copy kernel moves a
+// slice into a device slot on the copy stream, then the scatter kernel reads
+// the slot on the caller's stream.  Snapshot: the gather kernel fills the slot
+// on the caller's stream, then the copy stream copies it to the host image.  The slot's producer reuses
 // it only after its consumer is done with it.
 int run_ring(gms_manifest *m, int op, const HashOut &h, uint8_t *host_image, hipStream_t s)
 {
@@ -375,6 +375,8 @@ int run_ring(gms_manifest *m, int op, const HashOut &h, uint8_t *host_image, hip
         GMS_TRY(hipStreamWaitEvent(m->copy_stream, m->ev_done, 0));
         GMS_TRY(hipStreamWaitEvent(s, m->ev_done, 0));
     }
+    uint8_t *host_dev = nullptr;  // the pinned image as the copy kernel sees it
+    if (!to_host) GMS_TRY(hipHostGetDevicePointer((void **)&host_dev, host_image, 0));
     gms::RingFence fence(m, s);
     fence.armed = true;
     for (uint64_t sl = 0; sl < nslices; ++sl) {
@@ -386,7 +388,7 @@ int run_ring(gms_manifest *m, int op, const HashOut &h, uint8_t *host_image, hip
         if (to_host)
             GMS_TRY(gms::launch_slice(m, op, h, sl, dev, s));
         else
-            GMS_TRY(hipMemcpyAsync(dev, host_image + lo, bytes, hipMemcpyHostToDevice, m->copy_stream));
+            GMS_TRY(gms::launch_host_copy(host_dev + lo, dev, bytes, m->copy_stream));
         GMS_TRY(hipEventRecord(m->ev_filled[slot], producer));
         GMS_TRY(hipStreamWaitEvent(consumer, m->ev_filled[slot], 0));
         if (to_host)

@@ -11,8 +11,8 @@
 //
 // Restore runs a three-stage pipeline per staging slice: parallel workers move
 // the slice's pieces into a pinned host slot (pread, through per-worker
-// bounce buffers with O_DIRECT, or memcpy from a memory image), a DMA moves
-// that slot into a device slot on the manifest's copy stream, and the
+// bounce buffers with O_DIRECT, or memcpy from a memory image), a copy kernel
+// moves that slot into a device slot on the manifest's copy stream, and the
 // scatter(+hash) kernel runs on the caller's stream.  One pool of workers
 // takes pieces in image order from a shared counter, so every worker keeps a
 // large request in flight and none waits for a slower slice; a host slot is
@@ -338,6 +338,8 @@ int restore_pipeline(gms_manifest *m, const HostImage &src, const HashOut &h, un
     if ((rc = drain_ring(m)) != GMS_OK) return rc;
     const uint64_t slice = m->ring_slice;
     const uint32_t k = m->ring_slots, hk = m->host_slots;
+    uint8_t *h_dev = nullptr;  // the pinned host ring as the copy kernel sees it
+    GMS_TRY(hipHostGetDevicePointer((void **)&h_dev, m->h_ring, 0));
     GMS_TRY(hipEventRecord(m->ev_entry, s));
     GMS_TRY(hipStreamWaitEvent(m->copy_stream, m->ev_entry, 0));
     gms::RingFence fence(m, s);
@@ -348,13 +350,12 @@ int restore_pipeline(gms_manifest *m, const HostImage &src, const HashOut &h, un
     for (uint64_t sl = 0; sl < pool.nslices && rc == GMS_OK; ++sl) {
         if (!pool.wait_slice(sl)) break;  // a worker failed
         const uint32_t slot = (uint32_t)(sl % k), hslot = (uint32_t)(sl % hk);
-        uint8_t *host = m->h_ring + (uint64_t)hslot * slice;
         uint8_t *dev = m->d_ring + (uint64_t)slot * slice;
         const uint64_t lo = sl * slice;
         const uint64_t bytes = std::min(slice, m->image_bytes - lo);
         hipError_t e;
         if ((sl >= k && (e = hipStreamWaitEvent(m->copy_stream, m->ev_free[slot], 0)) != hipSuccess) ||
-            (e = hipMemcpyAsync(dev, host, bytes, hipMemcpyHostToDevice, m->copy_stream)) != hipSuccess ||
+            (e = gms::launch_host_copy(h_dev + (uint64_t)hslot * slice, dev, bytes, m->copy_stream)) != hipSuccess ||
             (e = hipEventRecord(m->ev_host[hslot], m->copy_stream)) != hipSuccess ||
             (e = hipEventRecord(m->ev_filled[slot], m->copy_stream)) != hipSuccess ||
             (e = hipStreamWaitEvent(s, m->ev_filled[slot], 0)) != hipSuccess ||

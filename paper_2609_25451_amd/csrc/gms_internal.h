@@ -34,6 +34,11 @@ struct HashOut {
     bool any() const { return blk || ten || expected; }
 };
 
+// Copies `bytes` (a multiple of 16) from `src`, pinned host memory mapped into
+// the device, to device memory `dst`, with a kernel on `s` rather than a DMA
+// engine.
+hipError_t launch_host_copy(const uint8_t *src, uint8_t *dst, uint64_t bytes, hipStream_t s);
+
 // Zeroes the tensor-hash array and the mismatch counter (either may be null).
 hipError_t launch_prologue(const HashOut &h, uint64_t n_entries, hipStream_t s);
 
