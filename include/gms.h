@@ -159,13 +159,15 @@ int gms_layout(const gms_manifest *m, uint64_t *img_off, uint64_t *blk_base);
 /*
  * Staging ring: `slots` device buffers of `slice_bytes` (rounded down to a
  * multiple of the chunk size, at least one chunk).  A restore from a pinned
- * host image DMAs host slices into free slots on a library-owned copy stream
+ * host image copies host slices into free slots with a copy kernel on a
+ * library-owned copy stream (a kernel rather than a DMA engine, whose rate
+ * drops for up to a second after device memory is remapped or re-allocated)
  * while the scatter kernel drains filled slots on the caller's stream; with
  * slots == 0 it reads the pinned image directly over the host link
  * (zero-copy) instead.  A snapshot into pinned host memory runs the other
  * way: the gather kernel fills a slot on the caller's stream and the copy
- * stream DMAs it to the host image; with slots == 0, or slices below 128 MiB
- * (where the device-to-host DMA loses half the link and more), it writes the
+ * stream copies it to the host image (hipMemcpyAsync); with slots == 0, or
+ * slices below 128 MiB (where those copies lose half the link and more), it writes the
  * image zero-copy.  The image-file and host-image calls also use the ring (and
  * a pinned host ring of twice the slots) and need slots > 0.  slice_bytes is 0, which selects
  * GMS_DEFAULT_SLICE_BYTES, or in [4096, 64 GiB]; slots at most 16; a new manifest starts with GMS_DEFAULT_SLICE_BYTES x
@@ -227,10 +229,10 @@ enum gms_file_flags {
  * packed image (the layout above, no header) starting at `file_offset`.
  * `io_threads` workers (0 = 16) read the image in pieces (16 MiB with
  * O_DIRECT, 64 MiB or one slice buffered), in file order, into the slices of
- * a pinned host ring; each full slice is DMA'd into
- * a device slot on the manifest's copy stream and scattered (and hashed /
+ * a pinned host ring; the copy kernel moves each full slice into
+ * a device slot on the manifest's copy stream and it is scattered (and hashed /
  * compared, as gms_restore) by the kernel on `stream`; a host slot is refilled
- * once its DMA has finished.  The call returns when every slice has been read
+ * once the copy out of it has finished.  The call returns when every slice has been read
  * and enqueued; device work completes on `stream`.  The first file call
  * allocates the manifest's pinned host ring: 2 x slots (at most 16) slices.
  * Errors: as gms_restore, plus GMS_ERR_IO (open/read failure) and
@@ -248,7 +250,7 @@ int gms_restore_from_file(const gms_manifest *m, const char *path, uint64_t file
 /*
  * Writes the packed image to `path` (created or truncated): the kernel gathers
  * each slice into a slot of the pinned host ring (through a device slot and a
- * DMA when slices are 128 MiB or more) and `io_threads` workers
+ * device-to-host copy when slices are 128 MiB or more) and `io_threads` workers
  * (0 = 16) write its 16 MiB pieces with pwrite; optionally emits the
  * block / tensor hashes of the gathered bytes.  Synchronous: the file is
  * complete when the call returns (durable too with GMS_FILE_SYNC).

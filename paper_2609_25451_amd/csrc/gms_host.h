@@ -18,7 +18,7 @@ constexpr uint64_t kDefaultSlice = GMS_DEFAULT_SLICE_BYTES;
 constexpr uint32_t kDefaultSlots = GMS_DEFAULT_SLOTS;
 constexpr uint32_t kMaxSlots = 16;
 constexpr uint64_t kMaxSlice = 64ull << 30;
-// Slices below this size make a snapshot's device-to-host DMA erratic (half the
+// Slices below this size make a snapshot's device-to-host copies erratic (half the
 // link and less with 64 MiB pieces); from 128 MiB up it holds about 99% of the
 // link, ahead of zero-copy stores from the gather kernel (about 96%).
 constexpr uint64_t kRingSnapshotMinSlice = 128ull << 20;
@@ -77,11 +77,11 @@ struct gms_manifest {
     uint64_t ring_slice = 0;
     uint32_t ring_slots = 0;
     uint8_t *h_ring = nullptr;  // pinned host slots (file paths only), host_slots x ring_slice
-    uint32_t host_slots = 0;    // twice the device slots (capped), so reads run ahead of the DMAs
+    uint32_t host_slots = 0;    // twice the device slots (capped), so reads run ahead of the link copies
     hipStream_t copy_stream = nullptr;
     hipEvent_t ev_filled[gms::kMaxSlots] = {};
     hipEvent_t ev_free[gms::kMaxSlots] = {};
-    hipEvent_t ev_host[gms::kMaxSlots] = {};  // DMA that last touched a host slot finished
+    hipEvent_t ev_host[gms::kMaxSlots] = {};  // link copy that last touched a host slot finished
     hipEvent_t ev_entry = nullptr;
     hipEvent_t ev_done = nullptr;
     bool done_recorded = false;

@@ -16,9 +16,9 @@
 // scatter(+hash) kernel runs on the caller's stream.  One pool of workers
 // takes pieces in image order from a shared counter, so every worker keeps a
 // large request in flight and none waits for a slower slice; a host slot is
-// refilled once the DMA that read it has finished, so the source, the host
+// refilled once the copy that read it has finished, so the source, the host
 // link and HBM all stay busy.  Snapshot runs the mirror image: the gather
-// kernel fills a slice (into a device slot that a DMA then copies to the host
+// kernel fills a slice (into a device slot that hipMemcpyAsync then copies to the host
 // slot, or straight into the host slot zero-copy when slices are small) and
 // the workers write its pieces out.
 
@@ -183,7 +183,7 @@ struct PiecePool {
 
 // Runs `threads` workers over the pool.  A worker takes piece p of slice s in
 // host slot s % hslots; to fill the slot (restore) it first waits until the
-// DMA out of that slot for slice s - hslots has been enqueued and has
+// copy out of that slot for slice s - hslots has been enqueued and has
 // finished; to drain it (snapshot) it waits until slice s has been enqueued
 // and has landed in the slot.
 class Workers {
@@ -374,7 +374,7 @@ int restore_pipeline(gms_manifest *m, const HostImage &src, const HashOut &h, un
 // Snapshot into a host image: the gather kernel fills each slice, which lands
 // in its pinned host slot, and the workers write the slot out.  With slices of
 // gms::kRingSnapshotMinSlice and up the kernel gathers into a device slot and
-// the copy stream DMAs it to the host slot; smaller slices are gathered
+// the copy stream copies it to the host slot; smaller slices are gathered
 // straight into the host slot over the link.  Returns when every byte is out.
 int snapshot_pipeline(gms_manifest *m, const HostImage &dst, const HashOut &h, unsigned threads, uint64_t piece,
                       hipStream_t s)

@@ -4,7 +4,7 @@ gms_snapshot_to_host gathers through the staging rings into a numpy buffer the
 library never pins; gms_restore_from_host copies a numpy image through the
 same rings into the entries.  Images, hashes, restored bytes (and the bytes
 around them) and mismatch lists are compared with the oracle over ring
-geometries that take both snapshot routes (device slot + DMA for slices of
+geometries that take both snapshot routes (device slot + device-to-host copy for slices of
 128 MiB and more, zero-copy into the host slot below), several worker counts,
 ring wrap-around and slice edges inside entries.
 """
@@ -69,7 +69,7 @@ def test_host_round_trip(staging, threads):
 
 def test_host_round_trip_across_128m_slices():
     """340 MiB over 128 MiB x 2 device slots (4 host slots): snapshots go through a device slot
-    and a DMA, the device ring wraps, and slice edges fall inside entries."""
+    and a device-to-host copy, the device ring wraps, and slice edges fall inside entries."""
     need_gpu()
     sizes = [(100 << 20) + 7, 13, (150 << 20) + 3 * 4096 + 5, 0, (90 << 20) + 4095]
     arena, datas = _setup(sizes, seed=52)

@@ -211,8 +211,8 @@ def test_ragged_manifest_pinned(staging):
 
 def test_pinned_snapshot_ring_across_slices():
     """A 340 MiB ragged image through 128 MiB x 2 slots: three slices, the ring wraps and slice
-    edges fall inside entries.  Snapshot (gather kernel into a device slot, DMA to the host
-    image), restore and verify equal the oracle; with 64 MiB slices the snapshot writes
+    edges fall inside entries.  Snapshot (gather kernel into a device slot, device-to-host copy to
+    the host image), restore and verify equal the oracle; with 64 MiB slices the snapshot writes
     zero-copy instead and gives the same image and hashes."""
     need_gpu()
     sizes = [(100 << 20) + 7, 13, (150 << 20) + 3 * 4096 + 5, 0, (90 << 20) + 4095]
