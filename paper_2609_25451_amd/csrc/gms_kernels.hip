@@ -316,12 +316,17 @@ k_pair(const Chunk *__restrict__ chunks, uint64_t count, gbyte *__restrict__ img
 // engine.  The copy stream's DMA engine is shared with work the driver starts
 // when device memory is remapped, or freed and allocated again, and for up to a
 // second then H2D DMAs ran at 34 to 46 of 57 GB/s; a kernel reading the pinned
-// slice over the link is not slowed.  64 workgroups, each taking 64 KiB spans in
-// turn with 16-byte non-temporal loads, keep enough reads in flight: 56.2 GB/s
-// on the llama8b ring restore against 55.9 GB/s with DMA; 256 or more
-// workgroups lose 2 to 3%.
+// slice over the link is not slowed.  32 workgroups, each taking 64 KiB spans in
+// turn with 16-byte non-temporal loads two deep per thread, keep 256 KiB of
+// host reads in flight: the link's bandwidth-latency product, and no more.
+// Every read beyond it only waits in queues that HBM traffic from other
+// kernels shares: with 1 MiB in flight (64 workgroups, four deep) the link
+// gained 0.2% while a device-image restore running beside the copy fell from
+// 81% to 28% of HBM peak; at 256 KiB it runs at 78%.  Grids that do not divide
+// the spans evenly (20, 24 or 48 workgroups) lose 2 to 3% of the link.
 constexpr uint32_t kCopyThreads = 256;
-constexpr uint32_t kCopyGroups = 64;
+constexpr uint32_t kCopyGroups = 32;
+constexpr int kCopyDepth = 2;                   // loads in flight per thread
 constexpr uint64_t kCopySpan = 64 * 1024 / 16;  // 16-byte elements per span
 
 __global__ void __launch_bounds__(kCopyThreads)
@@ -329,7 +334,7 @@ k_host_copy(const gvec *__restrict__ src, gvec *__restrict__ dst, uint64_t n16)
 {
     for (uint64_t lo = (uint64_t)blockIdx.x * kCopySpan; lo < n16; lo += (uint64_t)gridDim.x * kCopySpan) {
         const uint64_t hi = lo + kCopySpan < n16 ? lo + kCopySpan : n16;
-#pragma unroll 4
+#pragma unroll kCopyDepth
         for (uint64_t i = lo + threadIdx.x; i < hi; i += kCopyThreads) dst[i] = __builtin_nontemporal_load(src + i);
     }
 }
