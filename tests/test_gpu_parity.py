@@ -296,6 +296,45 @@ def test_corruption_flags_exact_blocks():
     assert int(to_u64(cnt)[0]) == want_cnt
 
 
+@pytest.mark.parametrize("chunks,tail", [(127, 0), (128, 0), (129, 0), (293, 5), (1025, 4097)],
+                         ids=["per127", "per128", "per129", "per294", "per1026"])
+def test_verify_unit_order_stripe_edges(chunks, tail):
+    """Verify walks units in 1 MiB stripes per XCD, with the last partial round of stripes split
+    into eight contiguous pieces.  One entry of `chunks` 64 KiB chunks (+ a ragged tail) gives a
+    launch whose grid holds exactly 8 slots per chunk, so each XCD's share of slots lands below, at
+    and above a stripe boundary.  A unit skipped or visited twice would change a block hash, the
+    tensor hash or the mismatch list against the oracle."""
+    need_gpu()
+    size = chunks * 65536 + tail
+    arena = Arena([size])
+    datas = random_datas([size], seed=chunks)
+    arena.fill(datas)
+    m = gms.Manifest(arena.entries, device=0, chunk_bytes=65536)
+    assert m.num_chunks == chunks + (tail > 0) and m.num_launch_groups == 1
+    o_blk, o_ten = oracle.hashes(datas)
+    nb = m.num_blocks
+    blk, ten = u64_dev(nb), u64_dev(1)
+    gms.verify(m, blk_hash=blk, ten_hash=ten)
+    torch.cuda.synchronize()
+    assert np.array_equal(to_u64(blk, nb), o_blk) and np.array_equal(to_u64(ten, 1), o_ten)
+    # corrupt the first block, a block of the last whole chunk and the last block
+    spots = sorted({0, (chunks - 1) * 65536 + 3 * 4096 + 17, size - 1})
+    bad = datas[0].copy()
+    v = arena.view(0)
+    for b in spots:
+        v[b:b + 1].bitwise_xor_(0x10)
+        bad[b] ^= 0x10
+    want_cnt, want = oracle.verify([bad], o_blk)
+    assert want_cnt == len(spots)
+    cnt, lst = u64_dev(1), u64_dev(8)
+    gms.verify(m, expected=from_u64(o_blk), blk_hash=blk, mismatch_count=cnt, mismatch_list=lst, mismatch_cap=8)
+    torch.cuda.synchronize()
+    c = int(to_u64(cnt)[0])
+    assert c == want_cnt and np.array_equal(np.sort(to_u64(lst, c)), want)
+    assert np.array_equal(to_u64(blk, nb), oracle.hashes([bad])[0])
+    m.close()
+
+
 def test_empty_and_zero_length_manifests():
     need_gpu()
     cnt = u64_dev(1)
