@@ -322,7 +322,10 @@ void gms_pool_destroy(gms_pool *p);
  * bytes above the pool's VA budget). */
 int gms_pool_alloc(gms_pool *p, uint64_t bytes, uint64_t align, uint64_t *addr_out);
 
-/* Returns an allocation; a dedicated mapping is unmapped and released, with its VA.
+/* Returns an allocation; a dedicated mapping is unmapped and released, with its VA,
+ * after the device has finished its work.  Slab space is handed to the next allocation
+ * at once, without waiting for the device: device work that still uses it must have
+ * finished, or be ordered before any use of the new allocation.
  * Errors: GMS_ERR_INVALID (not an allocation of this pool). */
 int gms_pool_free(gms_pool *p, uint64_t addr);
 
