@@ -249,8 +249,8 @@ __device__ __forceinline__ uint64_t xcd_slot()
 // contiguous pieces, which keeps the order a permutation of the round's slots.
 // Measured on the llama8b set over six image allocations: 90.4 to 91.8% of HBM
 // peak against 86.8 to 88.8% with contiguous eighths.  Restore and snapshot keep
-// the eighths: striping them gained on some workloads and lost 2.4 points on the
-// 70B shard.
+// the eighths: striping them narrowed their spread at the same mean on llama8b and
+// lost up to 2.9 points on the 70B shard.
 constexpr uint64_t kVerifyStripe = 128;
 
 __device__ __forceinline__ uint64_t striped_slot()
