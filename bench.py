@@ -30,8 +30,8 @@ sys.path.insert(0, ROOT)
 
 METRIC = "restore+verify GB/s on 1 GPU; seconds to restore a 16 GB weight shard"
 HBM_PEAK_GBS = 8000.0
-ALL_ROWS = ["main", "snapshot", "plain", "verify", "sequential", "tiny", "mixed", "h2d", "file", "kv", "kv_vmm", "store",
-            "recovery", "copy", "cpu", "shards"]
+ALL_ROWS = ["main", "snapshot", "plain", "verify", "sequential", "unaligned", "tiny", "mixed", "h2d", "file", "kv",
+            "kv_vmm", "store", "recovery", "copy", "cpu", "shards"]
 # What shapes the measured kernel's accesses: the kernel and its launch code, the
 # header's block and default chunk sizes and the chunking in manifest creation.
 KERNEL_SOURCES = ["paper_2609_25451_amd/csrc/gms_kernels.hip", "paper_2609_25451_amd/csrc/gms_internal.h"]
@@ -187,12 +187,9 @@ def settled(timer, fn, warm: int = 3, reps: int = 20):
 
 def build_weights(torch, synth, name):
     seed, specs = synth.weight_set(name)
-    tensors = []
-    for i, sp in enumerate(specs):
-        t = torch.empty(sp.shape, dtype=torch.bfloat16, device="cuda")
-        synth.dev_fill_bf16(t.data_ptr(), t.numel(), seed, i)
-        tensors.append(t)
+    tensors = [torch.empty(sp.shape, dtype=torch.bfloat16, device="cuda") for sp in specs]
     torch.cuda.synchronize()
+    synth.dev_fill_tensors(tensors, seed)  # one launch for the whole set
     return seed, specs, tensors
 
 
@@ -308,6 +305,8 @@ def main():
         result_rows["restore_then_verify_sequential"] = {
             "s": t, "GB_s": P / t / 1e9, "hbm_frac": (3 * P + 8 * nb) / t / 1e9 / HBM_PEAK_GBS,
             "fused_speedup": t / statistics.median(main_times) if main_times else None}
+    if "unaligned" in rows:
+        result_rows["unaligned"] = bench_unaligned(torch, gms, timer, tensors)
     if "tiny" in rows:
         result_rows["tiny"] = bench_tiny(torch, gms, synth, timer)
     if "mixed" in rows:
@@ -332,9 +331,9 @@ def main():
         # link peak: 1 GiB pinned -> device copies
         gib = pinned[: 1 << 30]
         dst = torch.empty(1 << 30, dtype=torch.uint8, device="cuda")
-        lt = timer.run(lambda: dst.copy_(gib, non_blocking=True), 10)
+        lt = timer.run(lambda: dst.copy_(gib, non_blocking=True), 20)
         link = (1 << 30) / statistics.median(lt) / 1e9
-        lt = timer.run(lambda: gib.copy_(dst, non_blocking=True), 10)
+        lt = timer.run(lambda: gib.copy_(dst, non_blocking=True), 20)
         link_d2h = (1 << 30) / statistics.median(lt) / 1e9
         del dst
         gms.snapshot(m, pinned, m.image_bytes, gms.MEM_HOST_PINNED)  # allocates the ring, untimed
@@ -404,7 +403,7 @@ def main():
     # ---------------------------------------------------------------- CPU oracle
     cpu = None
     if "cpu" in rows:
-        cpu = bench_cpu(torch, np, image, m, specs)
+        cpu = bench_cpu(torch, np, image, m, specs, expected)
 
     if "shards" in rows:  # last: frees the llama8b buffers to make room for the 122 GB MoE shard
         del tensors, image, expected, ten_hash, cnt, mlist
@@ -413,6 +412,23 @@ def main():
         torch.cuda.empty_cache()
         result_rows["shards"] = {name: bench_shard(torch, gms, synth, timer, name, link)
                                  for name in ("llama70b_tp8", "moe")}
+
+    # release the pinned and device buffers and join helper threads before the result line,
+    # so that the process has nothing left to tear down once it has reported
+    t_rel = time.perf_counter()
+    _PINNED["buf"] = None
+    if "shards" not in rows:  # the shard rows freed these already
+        del tensors, image, expected, ten_hash, cnt, mlist
+        m.close()
+    import gc
+
+    gc.collect()
+    torch.cuda.synchronize()
+    torch.cuda.empty_cache()
+    for t in threading.enumerate():
+        if t is not threading.current_thread() and not t.daemon:
+            t.join(timeout=30)
+    log(f"buffers released in {time.perf_counter() - t_rel:.2f} s")
 
     value = P * args.steps / wall / 1e9 if main_times else None
     out = {
@@ -526,6 +542,38 @@ def raw_direct_read(path, nbytes, threads=16, piece=16 << 20):
         os.close(fd)
 
 
+def bench_unaligned(torch, gms, timer, tensors, offset: int = 2):
+    """The llama8b tensors as entries 2 bytes past their start (each tensor minus its first
+    bf16 element), so every entry address is off a 16-byte boundary: the kernels' shifted
+    path.  Snapshot with hashes into an image of its own, then fused restore+verify (which
+    rewrites the same bytes) and verify alone."""
+    ents = [(t.data_ptr() + offset, t.numel() * t.element_size() - offset) for t in tensors]
+    mu = gms.Manifest(ents, device=0)
+    Pu, nbu = mu.payload_bytes, mu.num_blocks
+    img = torch.empty(mu.image_bytes, dtype=torch.uint8, device="cuda")
+    exp = torch.zeros(nbu, dtype=torch.int64, device="cuda")
+    c = torch.zeros(1, dtype=torch.int64, device="cuda")
+    with GpuSampler() as gs:
+        ts = settled(timer, lambda: gms.snapshot(mu, img, mu.image_bytes, blk_hash=exp))
+        tr = settled(timer, lambda: gms.restore(mu, img, mu.image_bytes, expected=exp, mismatch_count=c))
+    assert int(c.item()) == 0
+    tv = settled(timer, lambda: gms.verify(mu, expected=exp, mismatch_count=c))
+    assert int(c.item()) == 0
+    out = {"entry_offset_bytes": offset, "payload_bytes": Pu, "launch_groups": mu.num_launch_groups,
+           "restore_verify_s": tr, "restore_verify_GB_s": Pu / tr / 1e9,
+           "restore_verify_hbm_frac": (2 * Pu + 8 * nbu) / tr / 1e9 / HBM_PEAK_GBS,
+           "snapshot_hash_s": ts, "snapshot_hbm_frac": (2 * Pu + 8 * nbu) / ts / 1e9 / HBM_PEAK_GBS,
+           "verify_s": tv, "verify_hbm_frac": (Pu + 8 * nbu) / tv / 1e9 / HBM_PEAK_GBS, "gpu": gs.summary()}
+    log(f"unaligned (+{offset} B) llama8b: restore+verify {tr * 1e3:.2f} ms "
+        f"({out['restore_verify_hbm_frac'] * 100:.1f}% of HBM peak), snapshot {ts * 1e3:.2f} ms, "
+        f"verify {tv * 1e3:.2f} ms")
+    mu.close()
+    del img, exp
+    torch.cuda.synchronize()
+    torch.cuda.empty_cache()
+    return out
+
+
 def bench_tiny(torch, gms, synth, timer):
     """The tiny 21-tensor set (8.4 MB): it fits in the 256 MB last-level cache, so it is
     reported as latency, not against the HBM roofline."""
@@ -591,22 +639,38 @@ def bench_mixed(torch, gms, synth, timer, tensors, weights_s=None, n_small=200_0
 
 
 def host_info():
-    """CPU model, cores available to this process and NUMA nodes of the measuring host."""
-    model = ""
+    """The measuring host: the CPU as /proc/cpuinfo and lscpu describe it (a virtual machine may
+    show only a family name as the model), the CPUs this process may run on and NUMA nodes."""
+    info = {}
     try:
         with open("/proc/cpuinfo") as f:
             for line in f:
-                if line.startswith("model name"):
-                    model = line.split(":", 1)[1].strip()
+                key, _, val = line.partition(":")
+                key = key.strip()
+                if key in ("model name", "vendor_id", "cpu family", "model", "stepping", "cpu MHz", "cache size"):
+                    info.setdefault(key.replace(" ", "_"), val.strip())
+                if not line.strip() and info:
                     break
     except OSError:
+        pass
+    try:
+        import subprocess
+
+        out = subprocess.run(["lscpu"], capture_output=True, text=True, timeout=10).stdout
+        for line in out.splitlines():
+            key, _, val = line.partition(":")
+            if key.strip() in ("Model name", "BIOS Model name", "Socket(s)", "Core(s) per socket",
+                               "Thread(s) per core", "Hypervisor vendor", "L3 cache"):
+                info["lscpu_" + key.strip().replace(" ", "_").replace("(s)", "s")] = val.strip()
+    except (OSError, ValueError):
         pass
     nodes = 0
     try:
         nodes = len([d for d in os.listdir("/sys/devices/system/node") if d.startswith("node") and d[4:].isdigit()])
     except OSError:
         pass
-    return {"cpu_model": model, "cores_available": len(os.sched_getaffinity(0)), "numa_nodes": nodes}
+    return {"cpu_model": info.get("model_name", ""), "cpu": info, "cores_available": len(os.sched_getaffinity(0)),
+            "os_cpu_count": os.cpu_count(), "numa_nodes": nodes}
 
 
 def bench_kv(torch, np, gms, synth, timer, link=None):
@@ -949,64 +1013,77 @@ def bench_kv_vmm(torch, np, gms, synth, timer):
         pool.close()
 
 
-def bench_cpu(torch, np, image, m, specs, sample_bytes=8 << 30):
-    """The CPU oracle, as it stands, on a bounded sample of the same workload:
-    restore+verify (unpack, then block-hash compare) of whole tensors of the
-    image, about 8 GB of transformer layers (the tensors after the embedding
-    table, none larger than 117 MB).  Timed on one thread and on every core of
-    the machine's share (at most 16), the tensors spread over a thread pool
-    largest first; the oracle's C calls release the interpreter lock."""
+# Worker threads for the CPU oracle: the box grants each GPU a share of 16 CPUs, whatever
+# the affinity mask or os.cpu_count() show there.
+CPU_SHARE = 16
+
+
+def bench_cpu(torch, np, image, m, specs, expected):
+    """The CPU oracle, as it stands, over the whole llama8b set (291 tensors, 16.06 GB): a
+    snapshot (pack + block hashes of every tensor) and a restore+verify (unpack, then
+    block-hash compare against the snapshot's hashes), each timed as the median of 3 passes
+    on one thread and on the CPU share's threads, the tensors spread over a thread pool
+    largest first; the oracle's C calls release the interpreter lock.  The oracle's block
+    hashes of the whole set are also compared with the GPU snapshot's."""
     from concurrent.futures import ThreadPoolExecutor
 
     import oracle
 
     off, _ = m.layout()
-    k0 = k = 1
-    total = 0
-    while k < len(specs) and total < sample_bytes:
-        total += specs[k].nbytes
-        k += 1
-    pad = lambda n: -(-n // 4096) * 4096
-    lo, end = off[k0], off[k - 1] + pad(specs[k - 1].nbytes)
-    img = image[lo:end].cpu().numpy()
-    jobs = []
-    for i in range(k0, k):
-        n = specs[i].nbytes
-        jobs.append([img[off[i] - lo:off[i] - lo + pad(n)], np.empty(n, dtype=np.uint8), None])
-    jobs.sort(key=lambda j: -j[1].nbytes)
-    threads = max(1, min(16, len(os.sched_getaffinity(0))))
+    pad = lambda n: -(-n // 4096) * 4096  # noqa: E731
+    img = image.cpu().numpy()
+    total = sum(sp.nbytes for sp in specs)
+    jobs = [[img[off[i]:off[i] + pad(sp.nbytes)], np.empty(sp.nbytes, dtype=np.uint8), None]
+            for i, sp in enumerate(specs)]
+    order = sorted(range(len(jobs)), key=lambda i: -jobs[i][1].nbytes)
+    threads = max(1, min(CPU_SHARE, len(os.sched_getaffinity(0))))
 
     def expect(j):
         oracle.unpack_into(j[0], [j[1]])
         j[2] = oracle.hashes([j[1]])[0]
 
-    def one(j):
+    def restore_verify(j):
         oracle.unpack_into(j[0], [j[1]])
         return oracle.verify([j[1]], j[2])[0]
 
-    def passes(nthreads, reps):
+    def snapshot(j):
+        packed = oracle.pack([j[1]])
+        blk, _ = oracle.hashes([j[1]])
+        return int(packed.nbytes != j[0].nbytes or not np.array_equal(blk, j[2]))
+
+    def passes(fn, nthreads, reps=3):
         out = []
         for _ in range(reps):
             t0 = time.perf_counter()
             if nthreads == 1:
-                bad = sum(one(j) for j in jobs)
+                bad = sum(fn(jobs[i]) for i in order)
             else:
                 with ThreadPoolExecutor(nthreads) as ex:
-                    bad = sum(ex.map(one, jobs))
+                    bad = sum(ex.map(fn, [jobs[i] for i in order]))
             out.append(time.perf_counter() - t0)
             assert bad == 0
         return statistics.median(out)
 
     with ThreadPoolExecutor(threads) as ex:
-        list(ex.map(expect, jobs))
-    t1 = passes(1, 3)
-    tn = passes(threads, 5)
-    log(f"cpu oracle: {total} B in {t1:.2f} s on 1 thread, {tn:.2f} s on {threads} threads")
-    return {"value": round(total / tn / 1e9, 4), "unit": "GB/s", "cores": threads, "kind": "oracle",
-            "sample": f"restore+verify (unpack + block-hash compare) of {k - k0} whole tensors of the llama8b set "
-                      f"(tensors {k0}..{k - 1}, {total} B), {threads} threads over tensors, median of 5 passes",
-            "seconds": round(tn, 3), "single_thread_value": round(total / t1 / 1e9, 4),
-            "single_thread_seconds": round(t1, 3), "host": host_info()}
+        list(ex.map(expect, [jobs[i] for i in order]))
+    o_blk = np.concatenate([j[2] for j in jobs])
+    assert np.array_equal(o_blk, expected.cpu().numpy().view(np.uint64)), "oracle block hashes != GPU snapshot"
+    rv_n = passes(restore_verify, threads)
+    sn_n = passes(snapshot, threads)
+    rv_1 = passes(restore_verify, 1)
+    sn_1 = passes(snapshot, 1)
+    log(f"cpu oracle over {total} B: restore+verify {rv_1:.2f} s on 1 thread, {rv_n:.2f} s on {threads}; "
+        f"snapshot {sn_1:.2f} s / {sn_n:.2f} s")
+    del img, jobs
+    return {"value": round(total / rv_n / 1e9, 4), "unit": "GB/s", "cores": threads, "kind": "oracle",
+            "sample": f"restore+verify (unpack + block-hash compare) of the whole llama8b set ({len(specs)} tensors, "
+                      f"{total} B), {threads} threads over tensors, median of 3 passes",
+            "seconds": round(rv_n, 3), "single_thread_value": round(total / rv_1 / 1e9, 4),
+            "single_thread_seconds": round(rv_1, 3),
+            "snapshot": {"what": "pack + block hashes of every tensor", "seconds": round(sn_n, 3),
+                         "GB_s": round(total / sn_n / 1e9, 4), "single_thread_seconds": round(sn_1, 3),
+                         "single_thread_GB_s": round(total / sn_1 / 1e9, 4)},
+            "block_hashes_equal_gpu": True, "host": host_info()}
 
 
 if __name__ == "__main__":

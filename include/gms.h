@@ -195,8 +195,8 @@ int gms_snapshot(const gms_manifest *m, void *image, uint64_t image_bytes, int i
  * hashes of the restored bytes go to blk_hash_out, the tensor hashes to
  * ten_hash_out, and if expected_blk is given each block is compared with it;
  * mismatching global block indices are counted in *mismatch_count_out
- * (required when expected_blk is set; zeroed by the call) and the first
- * mismatch_cap of them written to mismatch_list_out.
+ * (required when expected_blk is set; zeroed by the call) and up to
+ * mismatch_cap of them, in any order, written to mismatch_list_out.
  * Errors: as gms_snapshot.
  */
 int gms_restore(const gms_manifest *m, const void *image, uint64_t image_bytes, int image_kind,
@@ -338,7 +338,9 @@ int gms_pool_release(gms_pool *p, uint64_t addr, uint64_t bytes);
 int gms_pool_remap(gms_pool *p, uint64_t addr, uint64_t bytes);
 
 /* Device access to the mapped mappings tiling [addr, addr+bytes): read_only != 0 maps
- * them read-only, 0 read-write.  Errors: GMS_ERR_INVALID, GMS_ERR_STATE (released). */
+ * them read-only, 0 read-write.  A switch to read-only first synchronizes the device, so
+ * writes that work on any stream still has in flight land before the pages turn read-only.
+ * Errors: GMS_ERR_INVALID, GMS_ERR_STATE (released). */
 int gms_pool_set_access(gms_pool *p, uint64_t addr, uint64_t bytes, int read_only);
 
 /* Pool facts (base: start of the placement window; reserved: the VA budget); any output
@@ -430,7 +432,8 @@ int gms_store_free(gms_store *s, uint64_t lease, uint64_t addr);
 
 /*
  * Writer only: commits entries[0..n) (each inside one allocation of the store) as the
- * layout, hashes its blocks and maps the pool read-only; the lease ends.  With
+ * layout, hashes its blocks, synchronizes the device (so device work of the writer on any
+ * stream has finished) and maps the pool read-only; the lease ends.  With
  * expected_blk (device, one u64 per block of the layout, as gms_snapshot writes them) the
  * populated contents must match it: on any mismatch the commit is refused with
  * GMS_ERR_INTEGRITY, *mismatch_count_out (host, may be NULL) holds the count, and the

@@ -147,6 +147,51 @@ def _ptr(x) -> int | None:
     return int(x)
 
 
+def _buf(x, need: int, what: str, words: bool = False) -> int | None:
+    """Pointer of an argument the library reads or writes ``need`` bytes of.  Tensors and
+    arrays are checked against their own size (the C side can only check the enclosing
+    allocation, which for a caching allocator is a whole segment); ``words`` arguments
+    must hold 64-bit integers.  Raw integer addresses pass unchecked."""
+    if x is None:
+        return None
+    if hasattr(x, "data_ptr"):
+        _dense(x)
+        es, nb = int(x.element_size()), int(x.numel() * x.element_size())
+        wordy = es == 8 and not x.is_floating_point() and not x.is_complex()
+        kind = str(x.dtype)
+    elif hasattr(x, "__array_interface__"):
+        if not x.flags["C_CONTIGUOUS"]:
+            raise ValueError(f"{what}: a non-contiguous array does not describe one byte range")
+        es, nb = int(x.dtype.itemsize), int(x.nbytes)
+        wordy = es == 8 and x.dtype.kind in "iu"
+        kind = str(x.dtype)
+    else:
+        return int(x)
+    if words and not wordy:
+        raise ValueError(f"{what}: needs 64-bit integer elements, got {kind}")
+    if nb < need:
+        raise ValueError(f"{what}: holds {nb} bytes, the call needs {need}")
+    return _ptr(x)
+
+
+def _image(x, image_bytes) -> tuple[int | None, int]:
+    """(pointer, byte count) of an image argument; a count given for a tensor or an array
+    must fit inside it."""
+    nb = _nbytes(x, image_bytes)
+    if hasattr(x, "data_ptr") or hasattr(x, "__array_interface__"):
+        have = _nbytes(x, None)
+        if nb > have:
+            raise ValueError(f"image: image_bytes {nb} exceeds the buffer's {have} bytes")
+    return _ptr(x), nb
+
+
+def _hash_args(m, expected, blk_hash, ten_hash, mismatch_count, mismatch_list, mismatch_cap):
+    nb, ne = m.num_blocks, m.num_entries
+    return (_buf(expected, nb * 8, "expected", True), _buf(blk_hash, nb * 8, "blk_hash", True),
+            _buf(ten_hash, ne * 8, "ten_hash", True), _buf(mismatch_count, 8, "mismatch_count", True),
+            _buf(mismatch_list, min(int(mismatch_cap), nb) * 8, "mismatch_list", True))
+
+
 def _nbytes(x, nbytes):
     if nbytes is not None:
         return int(nbytes)
@@ -274,36 +319,41 @@ class Manifest:
         _check(_set_staging(self._h, slice_bytes, slots), "gms_manifest_set_staging")
 
 
-def snapshot(m: Manifest, image, image_bytes: int, kind: int = MEM_DEVICE, blk_hash=None, ten_hash=None,
-             stream=None) -> None:
-    _check(_snapshot(m._h, _ptr(image), image_bytes, kind, _ptr(blk_hash), _ptr(ten_hash), _stream(stream)),
-           "gms_snapshot")
+def snapshot(m: Manifest, image, image_bytes: int | None = None, kind: int = MEM_DEVICE, blk_hash=None,
+             ten_hash=None, stream=None) -> None:
+    img, nb = _image(image, image_bytes)
+    _check(_snapshot(m._h, img, nb, kind, _buf(blk_hash, m.num_blocks * 8, "blk_hash", True),
+                     _buf(ten_hash, m.num_entries * 8, "ten_hash", True), _stream(stream)), "gms_snapshot")
 
 
-def restore(m: Manifest, image, image_bytes: int, kind: int = MEM_DEVICE, expected=None, blk_hash=None,
-            ten_hash=None, mismatch_count=None, mismatch_list=None, mismatch_cap: int = 0, stream=None) -> None:
-    _check(_restore(m._h, _ptr(image), image_bytes, kind, _ptr(expected), _ptr(blk_hash), _ptr(ten_hash),
-                    _ptr(mismatch_count), _ptr(mismatch_list), mismatch_cap, _stream(stream)), "gms_restore")
+def restore(m: Manifest, image, image_bytes: int | None = None, kind: int = MEM_DEVICE, expected=None,
+            blk_hash=None, ten_hash=None, mismatch_count=None, mismatch_list=None, mismatch_cap: int = 0,
+            stream=None) -> None:
+    img, nb = _image(image, image_bytes)
+    h = _hash_args(m, expected, blk_hash, ten_hash, mismatch_count, mismatch_list, mismatch_cap)
+    _check(_restore(m._h, img, nb, kind, *h, mismatch_cap, _stream(stream)), "gms_restore")
 
 
 def verify(m: Manifest, expected=None, blk_hash=None, ten_hash=None, mismatch_count=None, mismatch_list=None,
            mismatch_cap: int = 0, stream=None) -> None:
-    _check(_verify(m._h, _ptr(expected), _ptr(blk_hash), _ptr(ten_hash), _ptr(mismatch_count),
-                   _ptr(mismatch_list), mismatch_cap, _stream(stream)), "gms_verify")
+    h = _hash_args(m, expected, blk_hash, ten_hash, mismatch_count, mismatch_list, mismatch_cap)
+    _check(_verify(m._h, *h, mismatch_cap, _stream(stream)), "gms_verify")
 
 
 def restore_from_file(m: Manifest, path, file_offset: int = 0, flags: int = FILE_DIRECT, io_threads: int = 0,
                       expected=None, blk_hash=None, ten_hash=None, mismatch_count=None, mismatch_list=None,
                       mismatch_cap: int = 0, stream=None) -> None:
-    _check(_restore_file(m._h, os.fsencode(path), file_offset, flags, io_threads, _ptr(expected), _ptr(blk_hash),
-                         _ptr(ten_hash), _ptr(mismatch_count), _ptr(mismatch_list), mismatch_cap, _stream(stream)),
-           "gms_restore_from_file")
+    h = _hash_args(m, expected, blk_hash, ten_hash, mismatch_count, mismatch_list, mismatch_cap)
+    _check(_restore_file(m._h, os.fsencode(path), file_offset, flags, io_threads, *h, mismatch_cap,
+                         _stream(stream)), "gms_restore_from_file")
 
 
 def snapshot_to_file(m: Manifest, path, flags: int = 0, io_threads: int = 0, blk_hash=None, ten_hash=None,
                      stream=None) -> None:
-    _check(_snapshot_file(m._h, os.fsencode(path), flags, io_threads, _ptr(blk_hash), _ptr(ten_hash),
-                          _stream(stream)), "gms_snapshot_to_file")
+    _check(_snapshot_file(m._h, os.fsencode(path), flags, io_threads,
+                          _buf(blk_hash, m.num_blocks * 8, "blk_hash", True),
+                          _buf(ten_hash, m.num_entries * 8, "ten_hash", True), _stream(stream)),
+           "gms_snapshot_to_file")
 
 
 def restore_from_host(m: Manifest, image, image_bytes: int | None = None, threads: int = 0, expected=None,
@@ -311,16 +361,18 @@ def restore_from_host(m: Manifest, image, image_bytes: int | None = None, thread
                       stream=None) -> None:
     """Restore from an image in ordinary host memory (a numpy array, a CPU tensor or an
     address): returns once `image` may be reused; device work completes on `stream`."""
-    _check(_restore_host(m._h, _ptr(image), _nbytes(image, image_bytes), threads, _ptr(expected), _ptr(blk_hash),
-                         _ptr(ten_hash), _ptr(mismatch_count), _ptr(mismatch_list), mismatch_cap, _stream(stream)),
-           "gms_restore_from_host")
+    img, nb = _image(image, image_bytes)
+    h = _hash_args(m, expected, blk_hash, ten_hash, mismatch_count, mismatch_list, mismatch_cap)
+    _check(_restore_host(m._h, img, nb, threads, *h, mismatch_cap, _stream(stream)), "gms_restore_from_host")
 
 
 def snapshot_to_host(m: Manifest, image, image_bytes: int | None = None, threads: int = 0, blk_hash=None,
                      ten_hash=None, stream=None) -> None:
     """Snapshot into ordinary host memory; synchronous."""
-    _check(_snapshot_host(m._h, _ptr(image), _nbytes(image, image_bytes), threads, _ptr(blk_hash), _ptr(ten_hash),
-                          _stream(stream)), "gms_snapshot_to_host")
+    img, nb = _image(image, image_bytes)
+    _check(_snapshot_host(m._h, img, nb, threads, _buf(blk_hash, m.num_blocks * 8, "blk_hash", True),
+                          _buf(ten_hash, m.num_entries * 8, "ten_hash", True), _stream(stream)),
+           "gms_snapshot_to_host")
 
 
 class Pool:
@@ -428,8 +480,10 @@ class Store:
 
     def verify(self, mismatch_list=None, mismatch_cap: int = 0, stream=None) -> int:
         cnt = U64()
-        _check(_store_verify(self._h, ctypes.byref(cnt), _ptr(mismatch_list), mismatch_cap, _stream(stream)),
-               "gms_store_verify")
+        h = _store_layout(self._h)
+        nb = int(_num_blocks(h)) if h else 0
+        lst = _buf(mismatch_list, min(int(mismatch_cap), nb) * 8, "mismatch_list", True)
+        _check(_store_verify(self._h, ctypes.byref(cnt), lst, mismatch_cap, _stream(stream)), "gms_store_verify")
         return int(cnt.value)
 
     def layout(self) -> Manifest | None:
@@ -484,7 +538,9 @@ class WriteLease(_Lease):
     def commit(self, entries, expected=None, stream=None) -> None:
         ranges = _ranges(entries)
         cnt = U64()
-        rc = _store_commit(self._handle(), self.id, _entry_array(ranges), len(ranges), _ptr(expected),
+        nb = sum(-(-b // BLOCK_BYTES) for _, b in ranges)
+        rc = _store_commit(self._handle(), self.id, _entry_array(ranges), len(ranges),
+                           _buf(expected, nb * 8, "expected", True),
                            ctypes.byref(cnt), _stream(stream))
         if rc != GMS_OK:
             raise GmsError(rc, "gms_store_commit", int(cnt.value))

@@ -144,7 +144,10 @@ void plan_launch_groups(gms_manifest *m)
     // chunk that needs fewer units leaves the rest idle.  Walking the classes
     // from the largest down, a class gets a launch of its own (shared with the
     // smaller classes after it) once the idle units it would leave reach
-    // kSplitUnits; a manifest of similar chunks stays one launch.
+    // kSplitUnits; a manifest of similar chunks stays one launch.  Chunks of
+    // entries that are not 16-byte aligned then get launches of their own
+    // beside the aligned ones of the same size, so that each kernel carries
+    // only one of the two access paths.
     const uint64_t n = m->chunks.size();
     std::vector<uint8_t> cls(n);
     uint64_t count[kMaxUnitShift + 1] = {};
@@ -159,18 +162,27 @@ void plan_launch_groups(gms_manifest *m)
         group_of[s] = g;
         if (count[s] && (shifts.empty() || shifts.back() != g)) shifts.push_back(g);
     }
+    auto shifted = [&](uint64_t i) { return (m->chunks[i].addr & 15) != 0; };
+    bool present[kMaxUnitShift + 1][2] = {};
+    for (uint64_t i = 0; i < n; ++i) present[group_of[cls[i]]][shifted(i) ? 1 : 0] = true;
+    // groups: (shift, aligned) for each shift, largest first, aligned before shifted
+    std::vector<LaunchGroup> plan;
+    for (uint32_t sh : shifts)
+        for (int k = 0; k < 2; ++k)
+            if (present[sh][k]) plan.push_back(LaunchGroup{0, 0, sh, k == 1});
     m->groups.clear();
-    if (shifts.size() == 1) {
-        m->groups.push_back(LaunchGroup{0, n, shifts[0]});
+    if (plan.size() == 1) {
+        plan[0].count = n;
+        m->groups.push_back(plan[0]);
         return;
     }
-    // chunks by group, larger shift first, in image order within a group
+    // chunks by group, in image order within a group
     std::vector<Chunk> sorted;
     sorted.reserve(n);
-    for (uint32_t sh : shifts) {
-        LaunchGroup lg{sorted.size(), 0, sh};
+    for (LaunchGroup lg : plan) {
+        lg.first = sorted.size();
         for (uint64_t i = 0; i < n; ++i)
-            if (group_of[cls[i]] == sh) sorted.push_back(m->chunks[i]);
+            if (group_of[cls[i]] == lg.shift && shifted(i) == lg.shifted) sorted.push_back(m->chunks[i]);
         lg.count = sorted.size() - lg.first;
         m->groups.push_back(lg);
     }
@@ -180,7 +192,7 @@ void plan_launch_groups(gms_manifest *m)
 hipError_t launch_all(const gms_manifest *m, int op, const HashOut &h, uint8_t *img_base, hipStream_t s)
 {
     for (const LaunchGroup &g : m->groups) {
-        hipError_t e = launch_stream(op, h.any(), m->d_chunks, g.first, g.count, g.shift, img_base, 0, h, s);
+        hipError_t e = launch_stream(op, h.any(), g.shifted, m->d_chunks, g.first, g.count, g.shift, img_base, 0, h, s);
         if (e != hipSuccess) return e;
     }
     return hipSuccess;
@@ -192,7 +204,8 @@ hipError_t launch_slice(const gms_manifest *m, int op, const HashOut &h, uint64_
     for (size_t g = 0; g < m->groups.size(); ++g) {
         const uint64_t c0 = m->slice_first[g * stride + sl], c1 = m->slice_first[g * stride + sl + 1];
         hipError_t e =
-            launch_stream(op, h.any(), m->d_chunks, c0, c1 - c0, m->groups[g].shift, slot, sl * m->ring_slice, h, s);
+            launch_stream(op, h.any(), m->groups[g].shifted, m->d_chunks, c0, c1 - c0, m->groups[g].shift, slot,
+                          sl * m->ring_slice, h, s);
         if (e != hipSuccess) return e;
     }
     return hipSuccess;

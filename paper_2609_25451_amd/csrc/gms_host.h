@@ -51,10 +51,12 @@ struct DeviceGuard {
 
 namespace gms {
 // Chunks launched together: chunks[first, first + count), each needing at most
-// 2^shift work units.
+// 2^shift work units; `shifted` when their entry addresses are not 16-byte
+// aligned (all of them), clear when all are.
 struct LaunchGroup {
     uint64_t first = 0, count = 0;
     uint32_t shift = 0;
+    bool shifted = false;
 };
 }  // namespace gms
 

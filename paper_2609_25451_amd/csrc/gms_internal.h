@@ -45,8 +45,10 @@ hipError_t launch_prologue(const HashOut &h, uint64_t n_entries, hipStream_t s);
 // Runs `op` over chunks[first, first + count), each of which needs at most
 // 2^unit_shift work units of kBlocksPerUnit blocks (unit_shift <= kMaxUnitShift).
 // The image byte at offset x lives at img_base + (x - img_origin).  `hash`
-// selects the hashing variant.
-hipError_t launch_stream(int op, bool hash, const Chunk *chunks, uint64_t first, uint64_t count,
+// selects the hashing variant; `shifted` is set when the chunks' entry
+// addresses are not 16-byte aligned and clear when they all are (a launch
+// never mixes the two).
+hipError_t launch_stream(int op, bool hash, bool shifted, const Chunk *chunks, uint64_t first, uint64_t count,
                          uint32_t unit_shift, uint8_t *img_base, uint64_t img_origin, const HashOut &h,
                          hipStream_t s);
 

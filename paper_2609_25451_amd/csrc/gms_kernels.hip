@@ -18,8 +18,11 @@
 // one per chunk, from its wave).
 //
 // Bandwidth path: no MFMA; 16-byte non-temporal loads and stores for the
-// streaming side; byte-granular code only for unaligned entries and the ragged
-// last block of an entry.
+// streaming side, also for entries at any byte alignment (bytes are shifted
+// between lanes in registers); byte stores only where a partial 16-byte
+// granule has to be written.
+
+#include <cstdlib>
 
 #include "gms_internal.h"
 
@@ -99,10 +102,10 @@ __device__ __forceinline__ u32x4 keep_bytes(u32x4 v, uint32_t valid)
     return o;
 }
 
-// Reads `valid` bytes at p (any alignment), zero-extended to 16.
-__device__ __forceinline__ u32x4 load_part(const gbyte *p, uint32_t valid, bool aligned)
+// Reads `valid` bytes at the 16-byte-aligned p, zero-extended to 16.
+__device__ __forceinline__ u32x4 load_part(const gbyte *p, uint32_t valid)
 {
-    if (aligned && valid == 16) return *(const gvec *)p;
+    if (valid == 16) return *(const gvec *)p;
     uint64_t w0 = 0, w1 = 0;
     for (uint32_t q = 0; q < valid; ++q) {
         uint64_t b = p[q];
@@ -119,10 +122,10 @@ __device__ __forceinline__ u32x4 load_part(const gbyte *p, uint32_t valid, bool 
     return o;
 }
 
-// Writes the first `valid` bytes of v to p (any alignment).
-__device__ __forceinline__ void store_part(gbyte *p, u32x4 v, uint32_t valid, bool aligned)
+// Writes the first `valid` bytes of v to the 16-byte-aligned p.
+__device__ __forceinline__ void store_part(gbyte *p, u32x4 v, uint32_t valid)
 {
-    if (aligned && valid == 16) {
+    if (valid == 16) {
         __builtin_nontemporal_store(v, (gvec *)p);
         return;
     }
@@ -130,6 +133,69 @@ __device__ __forceinline__ void store_part(gbyte *p, u32x4 v, uint32_t valid, bo
     uint64_t w1 = (uint64_t)v.z | ((uint64_t)v.w << 32);
     for (uint32_t q = 0; q < valid; ++q)
         p[q] = (uint8_t)(q < 8 ? (w0 >> (8 * q)) : (w1 >> (8 * (q - 8))));
+}
+
+// Bytes o .. o + 15 (o = 1..15, wave-uniform) of the 32 bytes lo:hi, lo first.
+template <int D>
+__device__ __forceinline__ u32x4 join_at(u32x4 lo, u32x4 hi, uint32_t r)
+{
+    const uint32_t x[8] = {lo.x, lo.y, lo.z, lo.w, hi.x, hi.y, hi.z, hi.w};
+    u32x4 o;
+    o.x = __builtin_amdgcn_alignbyte(x[D + 1], x[D], r);
+    o.y = __builtin_amdgcn_alignbyte(x[D + 2], x[D + 1], r);
+    o.z = __builtin_amdgcn_alignbyte(x[D + 3], x[D + 2], r);
+    o.w = __builtin_amdgcn_alignbyte(x[D + 4], x[D + 3], r);
+    return o;
+}
+
+__device__ __forceinline__ u32x4 join(u32x4 lo, u32x4 hi, uint32_t o)
+{
+    switch (o >> 2) {  // uniform: the shift is fixed per chunk
+    case 0: return join_at<0>(lo, hi, o & 3);
+    case 1: return join_at<1>(lo, hi, o & 3);
+    case 2: return join_at<2>(lo, hi, o & 3);
+    default: return join_at<3>(lo, hi, o & 3);
+    }
+}
+
+__device__ __forceinline__ u32x4 shfl_up1(u32x4 v)  // lane l gets lane l - 1 (lane 0 its own)
+{
+    u32x4 o;
+    o.x = (uint32_t)__shfl_up((int)v.x, 1, 64);
+    o.y = (uint32_t)__shfl_up((int)v.y, 1, 64);
+    o.z = (uint32_t)__shfl_up((int)v.z, 1, 64);
+    o.w = (uint32_t)__shfl_up((int)v.w, 1, 64);
+    return o;
+}
+
+__device__ __forceinline__ u32x4 shfl_down1(u32x4 v)  // lane l gets lane l + 1 (lane 63 its own)
+{
+    u32x4 o;
+    o.x = (uint32_t)__shfl_down((int)v.x, 1, 64);
+    o.y = (uint32_t)__shfl_down((int)v.y, 1, 64);
+    o.z = (uint32_t)__shfl_down((int)v.z, 1, 64);
+    o.w = (uint32_t)__shfl_down((int)v.w, 1, 64);
+    return o;
+}
+
+__device__ __forceinline__ u32x4 read_lane(u32x4 v, int l)
+{
+    u32x4 o;
+    o.x = (uint32_t)__builtin_amdgcn_readlane((int)v.x, l);
+    o.y = (uint32_t)__builtin_amdgcn_readlane((int)v.y, l);
+    o.z = (uint32_t)__builtin_amdgcn_readlane((int)v.z, l);
+    o.w = (uint32_t)__builtin_amdgcn_readlane((int)v.w, l);
+    return o;
+}
+
+// Writes bytes [lo, hi) of v into the 16-byte-aligned granule p, byte by byte.
+__device__ __forceinline__ void store_granule(gbyte *p, u32x4 v, int lo, int hi)
+{
+#pragma unroll 1
+    for (int q = lo; q < hi; ++q) {
+        const uint32_t d = q < 4 ? v.x : q < 8 ? v.y : q < 12 ? v.z : v.w;
+        p[q] = (uint8_t)(d >> (8 * (q & 3)));
+    }
 }
 
 // Block epilogue.  `hl` is the lane's partial hash; with `check` set, lane 0
@@ -166,34 +232,134 @@ __device__ __forceinline__ void store_block(const u32x4 v[4], gbyte *p)
     for (int k = 0; k < 4; ++k) __builtin_nontemporal_store(v[k], (gvec *)(p + k * 1024));
 }
 
-// Full 4 KiB blocks a chunk can move with 16-byte accesses: all of them when
-// its entry address is 16-byte aligned, none otherwise.
-__device__ __forceinline__ uint32_t fast_blocks(const Chunk &c)
+// Block b of a chunk whose entry address is not 16-byte aligned (a = addr mod
+// 16, 1..15).  Image slots are 4096-aligned, so the image side stays in
+// 16-byte segments that hold whole entry words: lane l's segment s = 64k + l
+// holds entry bytes [16s, 16s + 16) of the block and is hashed exactly as on
+// the aligned path.  The entry side is covered by aligned 16-byte granules:
+// granule s starts a bytes before segment s, so it takes the last a bytes of
+// segment s - 1 and the first 16 - a of segment s, which the wave moves
+// between neighbouring lanes (lane 0 takes lane 63 of the previous k).  A
+// restore stores every granule that lies inside the block with one 16-byte
+// store; only the two granules the block shares with its neighbours, and
+// those past the entry's end, are written byte by byte, so no byte outside
+// the entry is touched.  Snapshot and verify load the granules that hold a
+// byte of the block (whole granules never leave the entry's pages) and shift
+// the other way.  Returns the block hash (in lane 0).
+template <int OP, bool HASH>
+__device__ __forceinline__ uint64_t move_block_shifted(const Chunk &c, uint32_t b, gbyte *img, uint64_t jg0,
+                                                       uint64_t gblk, const HashOut &h, uint32_t lane, bool check)
 {
-    return (c.addr & 15) == 0 ? c.len / kBlockBytes : 0;
+    const uint32_t a = (uint32_t)(c.addr & 15);
+    const uint32_t bs = b * kBlockBytes;
+    const int bv = (int)min(kBlockBytes, c.len - bs);            // real bytes of the block
+    gbyte *const gran = (gbyte *)(c.addr - a) + bs + lane * 16;  // the lane's granule of k = 0
+    u32x4 seg[4];
+    if (OP == kRestore) {
+#pragma unroll
+        for (int k = 0; k < 4; ++k) seg[k] = __builtin_nontemporal_load((const gvec *)(img + k * 1024));
+        // Whole granules are stored as they are formed.  The partial ones, at
+        // most two per block (the head, lane 0's granule 0, and the one holding
+        // the block's last byte), are kept and written once after the loop.
+        const u32x4 zero = {0u, 0u, 0u, 0u};
+        u32x4 head = zero, tail = zero;
+        int head_hi = 0, tail_hi = 0;
+        gbyte *tail_at = gran;
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+            u32x4 prev = shfl_up1(seg[k]);
+            if (k > 0) {
+                const u32x4 last = read_lane(seg[k - 1], 63);
+                if (lane == 0) prev = last;
+            }
+            const int s = 64 * k + (int)lane;
+            const int hi = min(16, bv + (int)a - 16 * s);
+            const u32x4 gv = join(prev, seg[k], 16 - a);
+            if (s == 0) {
+                head = gv;
+                head_hi = hi;
+            } else if (hi >= 16) {
+                __builtin_nontemporal_store(gv, (gvec *)(gran + k * 1024));
+            } else if (hi > 0) {
+                tail = gv;
+                tail_hi = hi;
+                tail_at = gran + k * 1024;
+            }
+        }
+        if (lane == 63 && bv + (int)a > (int)kBlockBytes) {  // the granule shared with the next block
+            tail = join(seg[3], zero, 16 - a);
+            tail_hi = bv + (int)a - (int)kBlockBytes;
+            tail_at = gran + 3 * 1024 + 16;
+        }
+        if (lane == 0) store_granule(gran, head, (int)a, head_hi);
+        if (tail_hi > 0) store_granule(tail_at, tail, 0, tail_hi);
+    } else {
+        u32x4 g[4];
+        const u32x4 zero = {0u, 0u, 0u, 0u};
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+            const int s = 64 * k + (int)lane;
+            g[k] = 16 * s < bv + (int)a ? __builtin_nontemporal_load((const gvec *)(gran + k * 1024)) : zero;
+        }
+        u32x4 tail = zero;
+        if (lane == 63 && bv + (int)a > (int)kBlockBytes) tail = *(const gvec *)(gran + 3 * 1024 + 16);
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+            u32x4 next = shfl_down1(g[k]);
+            if (k < 3) {
+                const u32x4 first = read_lane(g[k + 1], 0);
+                if (lane == 63) next = first;
+            } else if (lane == 63) {
+                next = tail;
+            }
+            const int s = 64 * k + (int)lane;
+            const uint32_t valid = (uint32_t)max(0, min(16, bv - 16 * s));
+            seg[k] = keep_bytes(join(g[k], next, a), valid);
+            if (OP == kSnapshot) __builtin_nontemporal_store(seg[k], (gvec *)(img + k * 1024));
+        }
+    }
+    uint64_t tacc = 0;
+    if (HASH) {
+        uint64_t hl = 0;
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+            const int s = 64 * k + (int)lane;
+            const int valid = max(0, min(16, bv - 16 * s));
+            const u32x4 v = OP == kRestore ? keep_bytes(seg[k], (uint32_t)valid) : seg[k];
+            const uint64_t jg = jg0 + (uint64_t)k * kSegStrideG;
+            const uint64_t w0 = (uint64_t)v.x | ((uint64_t)v.y << 32);
+            const uint64_t w1 = (uint64_t)v.z | ((uint64_t)v.w << 32);
+            if (valid > 0) hl ^= mix64(w0 ^ jg);
+            if (valid > 8) hl ^= mix64(w1 ^ (jg + kG));
+        }
+        tacc = finish_block(hl, gblk, h, lane, check, check ? h.expected[gblk] : 0);
+    }
+    return tacc;
 }
 
-// Block b of chunk c, by one wave.  A full, aligned block is loaded with
-// 16-byte non-temporal loads, stored and hashed from the same registers; its
-// expected hash is loaded branch-free (a harmless address when not checking)
-// just before its data and folded into the wave reduction.  The ragged last
-// block of an entry and every block of an unaligned entry take byte-granular
-// code.  Returns the block hash (in lane 0), or 0 past the chunk's end.
-template <int OP, bool HASH>
+// Block b of chunk c, by one wave.  Chunks of entries at a 16-byte-aligned
+// address (SHIFTED false; launches never mix the two kinds) move a full block
+// with 16-byte non-temporal loads, store and hash it from the same registers;
+// its expected hash is loaded branch-free (a harmless address when not
+// checking) just before its data and folded into the wave reduction.  The
+// ragged last block of an entry masks its partial segments.  Other chunks take
+// move_block_shifted.  Returns the block hash (in lane 0), or 0 past the
+// chunk's end.
+template <int OP, bool HASH, bool SHIFTED>
 __device__ __forceinline__ uint64_t move_block(const Chunk &c, uint32_t b, gbyte *img_base, uint64_t img_origin,
                                                const HashOut &h, uint32_t lane, bool check,
                                                const uint64_t *exp_dummy)
 {
     const uint32_t nblk = (c.len + kBlockBytes - 1) / kBlockBytes;
-    const uint32_t nfull = fast_blocks(c);
-    const bool aligned = (c.addr & 15) == 0;
     gbyte *const img = img_base + (c.img - img_origin) + (size_t)b * kBlockBytes + lane * 16;
     gbyte *const ent = (gbyte *)c.addr + (size_t)b * kBlockBytes + lane * 16;
     const uint64_t jg0 = (c.off >> 3) * kG + (uint64_t)b * kBlockStrideG + 2ull * lane * kG;
     const uint64_t gblk = (c.img >> 12) + b;
     uint64_t tacc = 0;
 
-    if (b < nfull) {  // full aligned block
+    if (SHIFTED) {
+        if (b < nblk) tacc = move_block_shifted<OP, HASH>(c, b, img, jg0, gblk, h, lane, check);
+    } else if (b < c.len / kBlockBytes) {  // full block
         uint64_t want = 0;
         if (HASH) want = *(check ? h.expected + gblk : exp_dummy);
         u32x4 v[4];
@@ -205,7 +371,7 @@ __device__ __forceinline__ uint64_t move_block(const Chunk &c, uint32_t b, gbyte
             for (int k = 0; k < 4; ++k) hl ^= seg_hash(v[k], jg0 + (uint64_t)k * kSegStrideG);
             tacc = finish_block(hl, gblk, h, lane, check, want);
         }
-    } else if (b < nblk) {  // ragged last block, or a block of an unaligned entry
+    } else if (b < nblk) {  // ragged last block
         const uint32_t boff = b * kBlockBytes;
         uint64_t hl = 0;
 #pragma unroll
@@ -215,9 +381,9 @@ __device__ __forceinline__ uint64_t move_block(const Chunk &c, uint32_t b, gbyte
             u32x4 v;
             if (OP == kRestore) {
                 v = keep_bytes(*(const gvec *)(img + k * 1024), valid);
-                store_part(ent + k * 1024, v, valid, aligned);
+                store_part(ent + k * 1024, v, valid);
             } else {
-                v = load_part(ent + k * 1024, valid, aligned);
+                v = load_part(ent + k * 1024, valid);
                 if (OP == kSnapshot) *(gvec *)(img + k * 1024) = v;
             }
             if (HASH) {
@@ -265,7 +431,7 @@ __device__ __forceinline__ uint64_t striped_slot()
 // (2^shift units cover the launch's longest chunk); wave w of the workgroup
 // takes the unit's block w.  Tensor hashes combine the two waves' block
 // hashes in LDS and take one atomic XOR per unit.
-template <int OP, bool HASH>
+template <int OP, bool HASH, bool SHIFTED>
 __global__ void __launch_bounds__(kUnitThreads)
 k_stream(const Chunk *__restrict__ chunks, uint64_t count, uint32_t unit_shift, gbyte *__restrict__ img_base,
          uint64_t img_origin, HashOut h)
@@ -283,7 +449,7 @@ k_stream(const Chunk *__restrict__ chunks, uint64_t count, uint32_t unit_shift, 
         if (u >= units) break;  // uniform across the workgroup
         const Chunk c = chunks[u >> unit_shift];
         const uint32_t b = ((uint32_t)u & unit_mask) * kWaves + wave;  // the wave's block of the chunk
-        const uint64_t tacc = move_block<OP, HASH>(c, b, img_base, img_origin, h, lane, check, exp_dummy);
+        const uint64_t tacc = move_block<OP, HASH, SHIFTED>(c, b, img_base, img_origin, h, lane, check, exp_dummy);
 
         // ---- tensor hash: XOR of the workgroup's block hashes, one atomic per unit
         if (HASH && h.ten) {
@@ -304,7 +470,7 @@ k_stream(const Chunk *__restrict__ chunks, uint64_t count, uint32_t unit_shift, 
 // one-block chunk would leave the unit's second wave idle, so instead wave w
 // of unit u takes all of chunk 2u + w, and each wave adds its chunk's hash to
 // the tensor hash itself.  No barrier: a wave past the last chunk just skips.
-template <int OP, bool HASH>
+template <int OP, bool HASH, bool SHIFTED>
 __global__ void __launch_bounds__(kUnitThreads)
 k_pair(const Chunk *__restrict__ chunks, uint64_t count, gbyte *__restrict__ img_base, uint64_t img_origin,
        HashOut h)
@@ -324,7 +490,7 @@ k_pair(const Chunk *__restrict__ chunks, uint64_t count, gbyte *__restrict__ img
         const uint32_t nblk = (c.len + kBlockBytes - 1) / kBlockBytes;  // at most kWaves
         uint64_t tacc = 0;
         for (uint32_t b = 0; b < nblk; ++b)
-            tacc ^= move_block<OP, HASH>(c, b, img_base, img_origin, h, lane, check, exp_dummy);
+            tacc ^= move_block<OP, HASH, SHIFTED>(c, b, img_base, img_origin, h, lane, check, exp_dummy);
         if (HASH && h.ten && lane == 0 && tacc)
             atomicXor((unsigned long long *)(h.ten + c.entry), (unsigned long long)tacc);
     }
@@ -367,7 +533,24 @@ k_prologue(uint64_t *__restrict__ ten, uint64_t n, uint64_t *__restrict__ mm_cou
     if (mm_count && tid == 0) *mm_count = 0;
 }
 
-constexpr uint64_t kMaxGrid = 1ull << 30;  // a multiple of kXcds
+// A dispatch counts its grid in work-items with 32 bits, so a launch holds at
+// most 2^24 workgroups of kUnitThreads (2^31 work-items, a multiple of kXcds);
+// larger launches loop over grid-sized rounds.  GMS_MAX_GRID (a multiple of 8,
+// read once) lowers the cap so that tests can run many rounds on small inputs.
+constexpr uint64_t kMaxGrid = 1ull << 24;
+static_assert(kMaxGrid * kUnitThreads <= (1ull << 32) - 1, "grid in work-items must fit 32 bits");
+
+uint64_t max_grid()
+{
+    static const uint64_t cap = [] {
+        const char *v = getenv("GMS_MAX_GRID");
+        if (!v || !*v) return kMaxGrid;
+        const unsigned long long x = strtoull(v, nullptr, 10);
+        if (x < kXcds || x > kMaxGrid || x % kXcds) return kMaxGrid;
+        return (uint64_t)x;
+    }();
+    return cap;
+}
 // Dynamic LDS per workgroup: restore and snapshot ask for a sixth of a CU's
 // 160 KiB so that six 2-wave workgroups are resident per CU; verify
 // (read-only, heavier on VALU per byte) only needs the wave partials and runs
@@ -378,21 +561,25 @@ constexpr uint64_t kMaxGrid = 1ull << 30;  // a multiple of kXcds
 constexpr size_t kLdsCopy = 26 * 1024;
 constexpr size_t kLdsVerify = kWaves * sizeof(uint64_t);
 
-uint64_t grid_for(uint64_t units) { return ((units < kMaxGrid ? units : kMaxGrid) + kXcds - 1) / kXcds * kXcds; }
+uint64_t grid_for(uint64_t units)
+{
+    const uint64_t cap = max_grid();
+    return ((units < cap ? units : cap) + kXcds - 1) / kXcds * kXcds;
+}
 
-template <int OP, bool HASH>
+template <int OP, bool HASH, bool SHIFTED>
 hipError_t launch_t(const Chunk *chunks, uint64_t first, uint64_t count, uint32_t unit_shift, uint8_t *img_base,
                     uint64_t img_origin, const HashOut &h, hipStream_t s)
 {
     if (unit_shift == 0) {
         const uint64_t grid = grid_for((count + kWaves - 1) / kWaves);
-        hipLaunchKernelGGL((k_pair<OP, HASH>), dim3((uint32_t)grid), dim3(kUnitThreads), 0, s, chunks + first, count,
+        hipLaunchKernelGGL((k_pair<OP, HASH, SHIFTED>), dim3((uint32_t)grid), dim3(kUnitThreads), 0, s, chunks + first, count,
                            (gbyte *)img_base, img_origin, h);
         return hipGetLastError();
     }
     constexpr size_t lds = OP == kVerify ? kLdsVerify : kLdsCopy;
     static_assert(lds <= 64 * 1024, "above 64 KiB the launch would have to opt in per device");
-    hipLaunchKernelGGL((k_stream<OP, HASH>), dim3((uint32_t)grid_for(count << unit_shift)), dim3(kUnitThreads), lds,
+    hipLaunchKernelGGL((k_stream<OP, HASH, SHIFTED>), dim3((uint32_t)grid_for(count << unit_shift)), dim3(kUnitThreads), lds,
                        s, chunks + first, count, unit_shift, (gbyte *)img_base, img_origin, h);
     return hipGetLastError();
 }
@@ -422,19 +609,27 @@ hipError_t launch_prologue(const HashOut &h, uint64_t n_entries, hipStream_t s)
     return hipGetLastError();
 }
 
-hipError_t launch_stream(int op, bool hash, const Chunk *chunks, uint64_t first, uint64_t count,
+template <bool SHIFTED>
+hipError_t launch_op(int op, bool hash, const Chunk *chunks, uint64_t first, uint64_t count, uint32_t shift,
+                     uint8_t *img_base, uint64_t img_origin, const HashOut &h, hipStream_t s)
+{
+    switch (op * 2 + (hash ? 1 : 0)) {
+    case kRestore * 2: return launch_t<kRestore, false, SHIFTED>(chunks, first, count, shift, img_base, img_origin, h, s);
+    case kRestore * 2 + 1: return launch_t<kRestore, true, SHIFTED>(chunks, first, count, shift, img_base, img_origin, h, s);
+    case kSnapshot * 2: return launch_t<kSnapshot, false, SHIFTED>(chunks, first, count, shift, img_base, img_origin, h, s);
+    case kSnapshot * 2 + 1: return launch_t<kSnapshot, true, SHIFTED>(chunks, first, count, shift, img_base, img_origin, h, s);
+    case kVerify * 2 + 1: return launch_t<kVerify, true, SHIFTED>(chunks, first, count, shift, img_base, img_origin, h, s);
+    default: return hipErrorInvalidValue;
+    }
+}
+
+hipError_t launch_stream(int op, bool hash, bool shifted, const Chunk *chunks, uint64_t first, uint64_t count,
                          uint32_t shift, uint8_t *img_base, uint64_t img_origin, const HashOut &h, hipStream_t s)
 {
     if (count == 0) return hipSuccess;
     if (shift > kMaxUnitShift || (count << shift) >> shift != count) return hipErrorInvalidValue;
-    switch (op * 2 + (hash ? 1 : 0)) {
-    case kRestore * 2: return launch_t<kRestore, false>(chunks, first, count, shift, img_base, img_origin, h, s);
-    case kRestore * 2 + 1: return launch_t<kRestore, true>(chunks, first, count, shift, img_base, img_origin, h, s);
-    case kSnapshot * 2: return launch_t<kSnapshot, false>(chunks, first, count, shift, img_base, img_origin, h, s);
-    case kSnapshot * 2 + 1: return launch_t<kSnapshot, true>(chunks, first, count, shift, img_base, img_origin, h, s);
-    case kVerify * 2 + 1: return launch_t<kVerify, true>(chunks, first, count, shift, img_base, img_origin, h, s);
-    default: return hipErrorInvalidValue;
-    }
+    return shifted ? launch_op<true>(op, hash, chunks, first, count, shift, img_base, img_origin, h, s)
+                   : launch_op<false>(op, hash, chunks, first, count, shift, img_base, img_origin, h, s);
 }
 
 }  // namespace gms

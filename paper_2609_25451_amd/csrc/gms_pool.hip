@@ -219,6 +219,11 @@ int pool_set_access_all(gms_pool *p, bool read_only)
     std::lock_guard<std::mutex> lock(p->mu);
     DeviceGuard g(p->device);
     if (g.err != hipSuccess) return fail_hip(g.err, "hipSetDevice");
+    // device writes still in flight, on any stream, must land before their pages turn read-only
+    if (read_only) {
+        hipError_t e = hipDeviceSynchronize();
+        if (e != hipSuccess) return fail_hip(e, "hipDeviceSynchronize");
+    }
     for (auto &kv : p->maps) {
         Mapping &m = kv.second;
         if (!m.mapped) continue;
@@ -430,9 +435,15 @@ int gms_pool_set_access(gms_pool *p, uint64_t addr, uint64_t bytes, int read_onl
     if (rc != GMS_OK) return rc;
     DeviceGuard g(p->device);
     if (g.err != hipSuccess) return fail_hip(g.err, "hipSetDevice");
+    for (uint64_t va : vas)
+        if (!p->maps[va].mapped) return fail(GMS_ERR_STATE, "mapping at %#llx is released", (unsigned long long)va);
+    // device writes still in flight, on any stream, must land before their pages turn read-only
+    if (read_only) {
+        hipError_t e = hipDeviceSynchronize();
+        if (e != hipSuccess) return fail_hip(e, "hipDeviceSynchronize");
+    }
     for (uint64_t va : vas) {
         Mapping &m = p->maps[va];
-        if (!m.mapped) return fail(GMS_ERR_STATE, "mapping at %#llx is released", (unsigned long long)va);
         if ((rc = set_access(p, va, m.bytes, read_only != 0)) != GMS_OK) return rc;
         m.read_only = read_only != 0;
     }

@@ -60,6 +60,8 @@ def _load_dev():
         lib.synth_dev_fill_bf16.restype = ctypes.c_int
         lib.synth_dev_fill_bytes.argtypes = [VP, U64, U64, U64, U64, VP]
         lib.synth_dev_fill_bytes.restype = ctypes.c_int
+        lib.synth_dev_fill_bf16_pieces.argtypes = [VP, U64, U64, VP]
+        lib.synth_dev_fill_bf16_pieces.restype = ctypes.c_int
         _dev = lib
     return _dev
 
@@ -115,3 +117,28 @@ def dev_fill_bytes(ptr: int, n: int, seed: int, stream_id: int, first: int = 0, 
     rc = _load_dev().synth_dev_fill_bytes(ptr, n, seed, stream_id, first, _stream_handle(stream))
     if rc != 0:
         raise RuntimeError(f"synth_dev_fill_bytes failed ({rc})")
+
+
+PIECE_ELEMS = 1 << 20  # elements per piece of a batched fill (2 MiB of bf16)
+
+
+def dev_fill_bf16_many(ranges, seed: int, stream=None) -> None:
+    """Fills device ranges [(address, elements, tensor id)] (elements 0.. of each tensor)
+    with one launch; returns once they are filled."""
+    rows = []
+    for ptr, n, tid in ranges:
+        for first in range(0, int(n), PIECE_ELEMS):
+            rows.append((int(ptr) + 2 * first, min(PIECE_ELEMS, int(n) - first), int(tid), first))
+    if not rows:
+        return
+    table = np.array(rows, dtype=np.uint64)
+    rc = _load_dev().synth_dev_fill_bf16_pieces(table.ctypes.data, len(rows), seed, _stream_handle(stream))
+    if rc != 0:
+        raise RuntimeError(f"synth_dev_fill_bf16_pieces failed ({rc})")
+
+
+def dev_fill_tensors(tensors, seed: int, ids=None, stream=None) -> None:
+    """Every tensor t_k gets the bf16 stream of tensor id ids[k] (default k), in one launch."""
+    ids = range(len(tensors)) if ids is None else ids
+    dev_fill_bf16_many([(t.data_ptr(), t.numel() * t.element_size() // 2, i) for t, i in zip(tensors, ids)],
+                       seed, stream)

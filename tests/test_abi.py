@@ -25,9 +25,10 @@ def test_exports_every_declared_symbol():
     assert gms.abi_version() == 3
 
 
-def _host_manifest(sizes, base=1 << 40, gap=0, chunk_bytes=0):
+def _host_manifest(sizes, base=1 << 40, gap=0, chunk_bytes=0, align=1):
     ents, a = [], base
     for s in sizes:
+        a = (a + align - 1) // align * align
         ents.append((a, s))
         a += s + gap
     return gms.Manifest(ents, device=gms.HOST_ONLY, chunk_bytes=chunk_bytes)
@@ -167,20 +168,77 @@ def test_launch_groups_split_only_when_idle_units_pay_for_a_launch():
     eight.  Tiny chunks beside large ones get a launch of their own once the idle units they would
     leave (7 each) reach 16,384; a manifest of similar chunks is a single launch."""
     big = [64 << 20] * 4
-    assert _host_manifest(big).num_launch_groups == 1
-    assert _host_manifest(big + [100] * 2340).num_launch_groups == 1  # 16,380 idle units
-    assert _host_manifest(big + [100] * 2341).num_launch_groups == 2  # 16,387
-    assert _host_manifest([100] * 200_000).num_launch_groups == 1
-    assert _host_manifest([]).num_launch_groups == 0
+    hm = lambda sizes: _host_manifest(sizes, align=256)  # noqa: E731  (torch-like 256-byte alignment)
+    assert hm(big).num_launch_groups == 1
+    assert hm(big + [100] * 2340).num_launch_groups == 1  # 16,380 idle units
+    assert hm(big + [100] * 2341).num_launch_groups == 2  # 16,387
+    assert hm([100] * 200_000).num_launch_groups == 1
+    assert hm([]).num_launch_groups == 0
     # a middle class too small to pay for a launch stays in the large chunks' launch
-    m = _host_manifest(big + [100] * 3000 + [20_000] * 10)  # 20,000 B: 5 blocks, 3 units -> 4
+    m = hm(big + [100] * 3000 + [20_000] * 10)  # 20,000 B: 5 blocks, 3 units -> 4
     assert m.num_launch_groups == 2
     # the weight sets and the KV pool
     for name, groups in (("tiny", 1), ("llama8b", 1), ("llama70b_tp8", 1), ("moe", 3)):
         _, ts = synth.weight_set(name)
-        assert _host_manifest([t.nbytes for t in ts]).num_launch_groups == groups, name
+        assert hm([t.nbytes for t in ts]).num_launch_groups == groups, name
+    # entries off a 16-byte boundary get launches of their own beside aligned ones of the same
+    # size class; a manifest of only one kind stays one launch per class
+    assert _host_manifest(big, base=(1 << 40) + 2).num_launch_groups == 1
+    assert _host_manifest([100] * 1000, base=(1 << 40) + 3, align=256).num_launch_groups == 1
+    assert _host_manifest([100] * 1000).num_launch_groups == 2  # 100-byte steps: a quarter aligned
+    assert _host_manifest(big + [100] * 3000, gap=2).num_launch_groups == 4
+    m = _host_manifest(big + [100] * 3000, gap=2)
+    assert m.image_bytes == hm(big + [100] * 3000).image_bytes
     # the layout does not depend on the grouping
     sizes = big + [100] * 3000
     m, m1 = _host_manifest(sizes), _host_manifest(sizes[:4])
     off, _ = m.layout()
     assert off[:4] == m1.layout()[0] and m.image_bytes == m1.image_bytes + 3000 * 4096
+
+
+def test_binding_refuses_short_or_mistyped_outputs():
+    """The C side can only check that a pointer range lies inside one allocation, and under a
+    caching allocator that is a whole segment; the binding therefore checks each tensor or
+    array against its own size and element type before the call (nothing reaches the library)."""
+    import torch
+
+    m = _host_manifest([5000, 3000, 0, 12_288])  # 2 + 1 + 0 + 3 blocks, 4 entries
+    nb, ne = m.num_blocks, m.num_entries
+    assert (nb, ne) == (6, 4)
+    short = [np.zeros(nb - 1, np.uint64), torch.zeros(nb - 1, dtype=torch.int64)]
+    mistyped = [np.zeros(nb, np.int32), np.zeros(nb, np.float64), torch.zeros(2 * nb, dtype=torch.int32),
+                torch.zeros(nb, dtype=torch.float64)]
+    for bad in short:
+        for call in (lambda: gms.verify(m, blk_hash=bad, stream=0),
+                     lambda: gms.verify(m, expected=bad, mismatch_count=np.zeros(1, np.uint64), stream=0),
+                     lambda: gms.snapshot(m, np.zeros(m.image_bytes, np.uint8), blk_hash=bad, stream=0),
+                     lambda: gms.restore(m, np.zeros(m.image_bytes, np.uint8), expected=bad,
+                                         mismatch_count=np.zeros(1, np.uint64), stream=0)):
+            with pytest.raises(ValueError, match="holds"):
+                call()
+    for bad in mistyped:
+        with pytest.raises(ValueError, match="64-bit integer"):
+            gms.verify(m, blk_hash=bad, stream=0)
+    with pytest.raises(ValueError, match="ten_hash"):
+        gms.verify(m, ten_hash=np.zeros(ne - 1, np.uint64), stream=0)
+    with pytest.raises(ValueError, match="mismatch_count"):
+        gms.verify(m, expected=np.zeros(nb, np.uint64), mismatch_count=np.zeros(0, np.uint64), stream=0)
+    # the list must hold min(cap, blocks) entries
+    with pytest.raises(ValueError, match="mismatch_list"):
+        gms.verify(m, expected=np.zeros(nb, np.uint64), mismatch_count=np.zeros(1, np.uint64),
+                   mismatch_list=np.zeros(3, np.uint64), mismatch_cap=4, stream=0)
+    # a claimed image size beyond the buffer
+    with pytest.raises(ValueError, match="image_bytes"):
+        gms.restore(m, np.zeros(m.image_bytes, np.uint8), m.image_bytes + 1, stream=0)
+    with pytest.raises(ValueError, match="image_bytes"):
+        gms.snapshot_to_host(m, torch.zeros(m.image_bytes - 1, dtype=torch.uint8), m.image_bytes, stream=0)
+    # well-formed outputs pass the binding and reach the library (which refuses a host-only manifest)
+    ok = dict(expected=np.zeros(nb, np.uint64), blk_hash=torch.zeros(nb, dtype=torch.int64),
+              ten_hash=np.zeros(ne, np.int64), mismatch_count=np.zeros(1, np.uint64),
+              mismatch_list=np.zeros(2, np.uint64), mismatch_cap=2)
+    with pytest.raises(gms.GmsError) as e:
+        gms.verify(m, stream=0, **ok)
+    assert e.value.status == gms.GMS_ERR_STATE
+    with pytest.raises(gms.GmsError) as e:
+        gms.restore(m, np.zeros(m.image_bytes, np.uint8), stream=0, **ok)
+    assert e.value.status == gms.GMS_ERR_STATE

@@ -1,11 +1,14 @@
-"""Full-size workloads, in the launch configuration bench.py times.
+"""Full-size workloads, in the launch configuration bench.py times, compared with
+the CPU oracle element by element.
 
-At these sizes the oracle checks sampled outputs one block at a time (the host
-regenerates the block's inputs with the seeded generator and hashes them);
-properties that hold at any size cover the rest: every restored tensor equals
-a fresh copy from the GPU generator (itself bit-identical to the host one),
-verify reproduces the snapshot hashes, dead KV units keep their poison, and a
-planted bit flip is flagged at exactly its block.
+Every workload streams through tests/full_parity.py: the seeded generator's
+bytes of each batch of entries go through the oracle, whose packed image must
+equal the library's image byte for byte and whose block and tensor hashes must
+equal every hash array the library produced (snapshot, fused restore, verify,
+pinned-host and pageable-host legs), whole arrays; the restored entries must
+equal the generator's bytes.  Mismatch counts and lists of planted bit flips
+are the oracle's verify of the flipped entry.  The KV pool's dead units must
+keep their poison.
 """
 import gc
 
@@ -16,17 +19,18 @@ import torch
 import oracle
 import paper_2609_25451_amd as gms
 import synth
+from full_parity import entry_bytes, weight_parity
 from gpu_util import need_gpu, to_u64
 
-pytestmark = pytest.mark.gpu
 
-SAMPLES = 40
+pytestmark = pytest.mark.gpu
 
 
 def _free():
     gc.collect()
     torch.cuda.synchronize()
     torch.cuda.empty_cache()
+    torch._C._host_emptyCache()  # pinned host blocks torch keeps cached for reuse
 
 
 def _alloc_or_skip(fn):
@@ -40,127 +44,108 @@ def _alloc_or_skip(fn):
 def _weights(name):
     seed, specs = synth.weight_set(name)
     ts = [torch.empty(sp.shape, dtype=torch.bfloat16, device="cuda") for sp in specs]
-    for i, t in enumerate(ts):
-        synth.dev_fill_bf16(t.data_ptr(), t.numel(), seed, i)
     torch.cuda.synchronize()
+    synth.dev_fill_tensors(ts, seed)  # one launch for the whole set
     return seed, specs, ts
 
 
-def _host_block(seed, tensor_id, nbytes, b):
-    """Host-generated bytes of 4 KiB block b of a bf16 tensor of nbytes."""
-    lo = b * 4096
-    hi = min(nbytes, lo + 4096)
-    return synth.bf16_bits((hi - lo) // 2, seed, tensor_id, first=lo // 2).view(np.uint8)
+def _weight_gen(seed, sizes):
+    """gen(lo, hi, dst): generator bytes of tensors lo..hi-1 (bf16 stream k for tensor k)."""
+    def gen(lo, hi, dst):
+        ranges, o = [], 0
+        for k in range(lo, hi):
+            ranges.append((dst.data_ptr() + o, sizes[k] // 2, k))
+            o += sizes[k]
+        synth.dev_fill_bf16_many(ranges, seed)
+    return gen
 
 
-def _sampled_blocks(sizes, base, rng, k=SAMPLES):
-    nblk = [-(-s // 4096) for s in sizes]
-    out = []
-    for _ in range(k):
-        i = int(rng.integers(0, len(sizes)))
-        while nblk[i] == 0:
-            i = int(rng.integers(0, len(sizes)))
-        b = int(rng.choice([0, nblk[i] - 1, int(rng.integers(0, nblk[i]))]))
-        out.append((i, b, base[i] + b))
-    return out
+def _restored(ts):
+    def cat(lo, hi):
+        return torch.cat([ts[k].view(torch.uint8).reshape(-1) for k in range(lo, hi)])
+    return cat
 
 
-def _equals_generated(ts, seed, ids=None):
-    """Every tensor equals a fresh GPU-generated copy (all bytes, any size)."""
-    biggest = max(t.numel() for t in ts)
-    scratch = torch.empty(biggest, dtype=torch.int16, device="cuda")
-    bad = []
-    for k, t in enumerate(ts):
-        tid = k if ids is None else ids[k]
-        n = t.numel()
-        synth.dev_fill_bf16(scratch.data_ptr(), n, seed, tid)
-        if not torch.equal(t.view(torch.int16).reshape(-1), scratch[:n]):
-            bad.append(tid)
-    del scratch
-    return bad
+def _oracle_flip(gen, sizes, base, o_blk, i, byte, mask):
+    """The oracle's verify of entry i with one bit flipped: (count, ascending global indices)."""
+    x = entry_bytes(gen, sizes, i)
+    x[byte] ^= mask
+    nb = -(-sizes[i] // 4096)
+    cnt, lst = oracle.verify([x], o_blk[base[i]:base[i] + nb])
+    return cnt, [int(v) + base[i] for v in lst], oracle.entry_hashes(x)[0]
 
 
+def _u64(t):
+    torch.cuda.synchronize()
+    return to_u64(t)
+
+
+@pytest.mark.timeout(900)
 @pytest.mark.parametrize("name", ["llama8b", "llama70b_tp8"])
 def test_full_weight_set(name):
     need_gpu()
     _free()
     seed, specs, ts = _alloc_or_skip(lambda: _weights(name))
     sizes = [sp.nbytes for sp in specs]
+    gen = _weight_gen(seed, sizes)
     m = gms.Manifest(ts, device=0)
     _, _, o_ib, o_nb = oracle.layout(sizes)
     assert m.image_bytes == o_ib and m.num_blocks == o_nb
     off, base = m.layout()
     img = _alloc_or_skip(lambda: torch.empty(m.image_bytes, dtype=torch.uint8, device="cuda"))
-    blk = torch.zeros(m.num_blocks, dtype=torch.int64, device="cuda")
-    ten = torch.zeros(m.num_entries, dtype=torch.int64, device="cuda")
+    z = lambda n: torch.zeros(n, dtype=torch.int64, device="cuda")  # noqa: E731
+    blk, ten, blk2, ten2, blk3, ten3 = z(m.num_blocks), z(m.num_entries), z(m.num_blocks), z(m.num_entries), \
+        z(m.num_blocks), z(m.num_entries)
+    cnt = torch.full((1,), 99, dtype=torch.int64, device="cuda")
     gms.snapshot(m, img, m.image_bytes, blk_hash=blk, ten_hash=ten)
-    torch.cuda.synchronize()
-
-    # sampled blocks: image bytes and block hashes against the oracle
-    rng = np.random.default_rng(sum(map(ord, name)))
-    hblk = to_u64(blk)
-    for i, b, g in _sampled_blocks(sizes, base, rng):
-        want = _host_block(seed, i, sizes[i], b)
-        got = img[off[i] + b * 4096: off[i] + b * 4096 + 4096].cpu().numpy()
-        assert np.array_equal(got[: want.size], want) and not got[want.size:].any(), f"image block {g}"
-        assert int(hblk[g]) == oracle.block_hash_at(want, sizes[i], b), f"block hash {g}"
-    # whole-tensor hashes of the small tensors (norms) by the oracle
-    hten = to_u64(ten)
-    for i, sp in enumerate(specs):
-        if sp.nbytes <= 64 * 1024:
-            _, t_o = oracle.entry_hashes(synth.bf16_bits(sp.numel, seed, i).view(np.uint8))
-            assert int(hten[i]) == t_o, f"tensor hash {i}"
-    # tensor hash == XOR of its block hashes, for every tensor
-    for i in range(len(specs)):
-        nbk = -(-sizes[i] // 4096)
-        assert int(np.bitwise_xor.reduce(hblk[base[i]:base[i] + nbk])) == int(hten[i])
-
-    # poison, fused restore+verify, compare every byte with the generator
     for t in ts:
         t.view(torch.uint8).fill_(0xA5)
-    cnt = torch.full((1,), 99, dtype=torch.int64, device="cuda")
-    blk2 = torch.zeros_like(blk)
-    gms.restore(m, img, m.image_bytes, expected=blk, blk_hash=blk2, mismatch_count=cnt)
-    torch.cuda.synchronize()
-    assert int(cnt.item()) == 0 and torch.equal(blk, blk2)
-    assert _equals_generated(ts, seed) == []
+    gms.restore(m, img, m.image_bytes, expected=blk, blk_hash=blk2, ten_hash=ten2, mismatch_count=cnt)
+    assert int(cnt.item()) == 0
+    gms.verify(m, expected=blk, blk_hash=blk3, ten_hash=ten3, mismatch_count=cnt)
+    assert int(cnt.item()) == 0
 
-    # verify reproduces the snapshot hashes; a planted bit flip is flagged exactly
-    blk3, ten3 = torch.zeros_like(blk), torch.zeros_like(ten)
-    gms.verify(m, blk_hash=blk3, ten_hash=ten3, expected=blk, mismatch_count=cnt)
-    torch.cuda.synchronize()
-    assert int(cnt.item()) == 0 and torch.equal(blk3, blk) and torch.equal(ten3, ten)
+    # the pinned-host image through the staging ring: snapshot, poison, restore
+    pinned = torch.empty(m.image_bytes, dtype=torch.uint8, pin_memory=True)
+    blk_ps, blk_pr = z(m.num_blocks), z(m.num_blocks)
+    gms.snapshot(m, pinned, m.image_bytes, gms.MEM_HOST_PINNED, blk_hash=blk_ps)
+    for t in ts:
+        t.view(torch.uint8).fill_(0xA5)
+    gms.restore(m, pinned, m.image_bytes, gms.MEM_HOST_PINNED, expected=blk, blk_hash=blk_pr, mismatch_count=cnt)
+    assert int(cnt.item()) == 0
+
+    # every image byte, block hash and tensor hash against the oracle; restored bytes
+    o_blk, o_ten = weight_parity(
+        m, sizes, gen, {"device": img, "pinned": pinned},
+        {"snapshot": _u64(blk), "restore": _u64(blk2), "verify": _u64(blk3), "pinned snapshot": _u64(blk_ps),
+         "pinned restore": _u64(blk_pr)},
+        {"snapshot": _u64(ten), "restore": _u64(ten2), "verify": _u64(ten3)},
+        restored=_restored(ts))
+    del pinned
+    _free()
+
+    # a planted bit flip in the image: the mismatch list is the oracle's verify of that entry
+    rng = np.random.default_rng(sum(map(ord, name)))
     i = int(rng.integers(0, len(ts)))
     byte = int(rng.integers(0, sizes[i]))
     img[off[i] + byte] ^= 0x04
     lst = torch.zeros(4, dtype=torch.int64, device="cuda")
-    gms.restore(m, img, m.image_bytes, expected=blk, mismatch_count=cnt, mismatch_list=lst, mismatch_cap=4)
-    torch.cuda.synchronize()
-    assert int(cnt.item()) == 1 and int(lst[0].item()) == base[i] + byte // 4096
+    blk_f = z(m.num_blocks)
+    gms.restore(m, img, m.image_bytes, expected=blk, blk_hash=blk_f, mismatch_count=cnt, mismatch_list=lst,
+                mismatch_cap=4)
+    o_cnt, o_lst, o_flipped = _oracle_flip(gen, sizes, base, o_blk, i, byte, 0x04)
+    assert int(cnt.item()) == o_cnt == 1 and sorted(_u64(lst)[:1].tolist()) == o_lst
+    want = o_blk.copy()
+    want[base[i]:base[i] + o_flipped.size] = o_flipped
+    assert np.array_equal(_u64(blk_f), want)
     img[off[i] + byte] ^= 0x04
     gms.restore(m, img, m.image_bytes)  # the tensors took the flipped bit; restore the clean image
-
-    if name == "llama8b":
-        # host-pinned image through the staging ring
-        pinned = torch.empty(m.image_bytes, dtype=torch.uint8, pin_memory=True)
-        gms.snapshot(m, pinned, m.image_bytes, gms.MEM_HOST_PINNED)
-        torch.cuda.synchronize()
-        for i, b, g in _sampled_blocks(sizes, base, rng, k=16):
-            want = _host_block(seed, i, sizes[i], b)
-            got = pinned[off[i] + b * 4096: off[i] + b * 4096 + 4096].numpy()
-            assert np.array_equal(got[: want.size], want) and not got[want.size:].any()
-        for t in ts:
-            t.view(torch.uint8).fill_(0xA5)
-        gms.restore(m, pinned, m.image_bytes, gms.MEM_HOST_PINNED, expected=blk, mismatch_count=cnt)
-        torch.cuda.synchronize()
-        assert int(cnt.item()) == 0
-        assert _equals_generated(ts, seed) == []
-        del pinned
     m.close()
-    del ts, img, blk, blk2, blk3, ten, ten3
+    del ts, img, blk, blk2, blk3, ten, ten2, ten3, blk_ps, blk_pr, blk_f
     _free()
 
 
+@pytest.mark.timeout(900)
 def test_full_kv_pool_live_blocks_and_corruption():
     need_gpu()
     _free()
@@ -170,104 +155,151 @@ def test_full_kv_pool_live_blocks_and_corruption():
     for l, t in enumerate(pool):
         synth.dev_fill_bf16(t.data_ptr(), p.layer_bytes // 2, p.seed, l)
     live = synth.live_map(p.blocks, p.n_live, p.map_seed, p.map_stream)
+    live_t = torch.from_numpy(live.astype(np.int64)).cuda()
     ents = [(pool[l].data_ptr() + int(b) * p.unit_bytes, p.unit_bytes) for l in range(p.layers) for b in live]
     m = gms.Manifest(ents, device=0)
     assert m.num_entries == 78_624 and m.payload_bytes == 5_152_702_464
+    sizes = [p.unit_bytes] * m.num_entries
     off, base = m.layout()
+    layer = torch.empty(p.layer_bytes, dtype=torch.uint8, device="cuda")
+
+    def gen(lo, hi, dst):  # generator bytes of live units lo..hi-1 (layer-major, ids ascending)
+        o, e = 0, lo
+        while e < hi:
+            l, j0 = divmod(e, p.n_live)
+            j1 = min(p.n_live, j0 + hi - e)
+            synth.dev_fill_bf16(layer.data_ptr(), p.layer_bytes // 2, p.seed, l)
+            u = layer.view(p.blocks, p.unit_bytes)[live_t[j0:j1]].reshape(-1)
+            dst[o:o + u.numel()].copy_(u)
+            o, e = o + u.numel(), e + j1 - j0
+
+    def restored(lo, hi):
+        parts, e = [], lo
+        while e < hi:
+            l, j0 = divmod(e, p.n_live)
+            j1 = min(p.n_live, j0 + hi - e)
+            parts.append(pool[l].view(p.blocks, p.unit_bytes)[live_t[j0:j1]].reshape(-1))
+            e += j1 - j0
+        return torch.cat(parts)
+
+    z = lambda n: torch.zeros(n, dtype=torch.int64, device="cuda")  # noqa: E731
     img = torch.empty(m.image_bytes, dtype=torch.uint8, device="cuda")
-    exp = torch.zeros(m.num_blocks, dtype=torch.int64, device="cuda")
-    gms.snapshot(m, img, m.image_bytes, blk_hash=exp)
-    torch.cuda.synchronize()
+    exp, ten, blk2 = z(m.num_blocks), z(m.num_entries), z(m.num_blocks)
+    cnt = torch.zeros(1, dtype=torch.int64, device="cuda")
+    lst = torch.zeros(8, dtype=torch.int64, device="cuda")
+    gms.snapshot(m, img, m.image_bytes, blk_hash=exp, ten_hash=ten)
+    for t in pool:
+        t.fill_(0xA5)
+    gms.restore(m, img, m.image_bytes, expected=exp, blk_hash=blk2, mismatch_count=cnt)
+    assert int(cnt.item()) == 0
+    dead = torch.from_numpy(np.setdiff1d(np.arange(p.blocks), live)).cuda()
+    for l, t in enumerate(pool):
+        assert bool((t.view(p.blocks, p.unit_bytes)[dead] == 0xA5).all()), f"layer {l}: a dead unit was written"
 
-    # sampled oracle checks: unit bytes and block hashes
-    rng = np.random.default_rng(5)
-    hexp = to_u64(exp)
-    for _ in range(SAMPLES):
-        e = int(rng.integers(0, m.num_entries))
-        layer, bid = e // p.n_live, int(live[e % p.n_live])
-        blkno = int(rng.integers(0, 16))
-        first = (bid * p.unit_bytes + blkno * 4096) // 2
-        want = synth.bf16_bits(2048, p.seed, layer, first=first).view(np.uint8)
-        got = img[off[e] + blkno * 4096: off[e] + blkno * 4096 + 4096].cpu().numpy()
-        assert np.array_equal(got, want)
-        assert int(hexp[base[e] + blkno]) == oracle.block_hash_at(want, p.unit_bytes, blkno)
+    # whole image, block and tensor hashes against the oracle; restored live units
+    o_blk, o_ten = weight_parity(m, sizes, gen, {"device": img}, {"snapshot": _u64(exp), "restore": _u64(blk2)},
+                                 {"snapshot": _u64(ten)}, restored=restored)
 
-    # planted corruption in the image, seeded
+    # the planted corruption (seeded), in the image: the oracle's verify decides the list
     e = synth.u64(p.corrupt_seed, p.corrupt_stream, 0) % m.num_entries
     bl = synth.u64(p.corrupt_seed, p.corrupt_stream, 1) % 16
     bit = synth.u64(p.corrupt_seed, p.corrupt_stream, 2) % (4096 * 8)
-    img[off[e] + bl * 4096 + bit // 8] ^= 1 << (bit % 8)
+    byte, mask = bl * 4096 + bit // 8, 1 << (bit % 8)
+    o_cnt, o_lst, o_flipped = _oracle_flip(gen, sizes, base, o_blk, e, byte, mask)
+    want = o_blk.copy()
+    want[base[e]:base[e] + 16] = o_flipped
+    img[off[e] + byte] ^= mask
     for t in pool:
         t.fill_(0xA5)
-    cnt = torch.zeros(1, dtype=torch.int64, device="cuda")
-    lst = torch.zeros(8, dtype=torch.int64, device="cuda")
-    gms.restore(m, img, m.image_bytes, expected=exp, mismatch_count=cnt, mismatch_list=lst, mismatch_cap=8)
-    torch.cuda.synchronize()
-    assert int(cnt.item()) == 1 and int(lst[0].item()) == base[e] + bl
-
-    # live units hold their data (bar the flipped bit); dead units keep the poison
-    dead = torch.from_numpy(np.setdiff1d(np.arange(p.blocks), live)).cuda()
-    livet = torch.from_numpy(live.astype(np.int64)).cuda()
-    scratch = torch.empty(p.layer_bytes, dtype=torch.uint8, device="cuda")
-    flip_layer, flip_unit = e // p.n_live, int(live[e % p.n_live])
+    blk_f = z(m.num_blocks)
+    gms.restore(m, img, m.image_bytes, expected=exp, blk_hash=blk_f, mismatch_count=cnt, mismatch_list=lst,
+                mismatch_cap=8)
+    assert int(cnt.item()) == o_cnt == 1 and _u64(lst)[:1].tolist() == o_lst == [base[e] + bl]
+    assert np.array_equal(_u64(blk_f), want)
     for l, t in enumerate(pool):
-        u = t.view(p.blocks, p.unit_bytes)
-        assert bool((u[dead] == 0xA5).all()), f"layer {l}: a dead unit was written"
-        synth.dev_fill_bf16(scratch.data_ptr(), p.layer_bytes // 2, p.seed, l)
-        if l == flip_layer:
-            scratch.view(p.blocks, p.unit_bytes)[flip_unit, bl * 4096 + bit // 8] ^= 1 << (bit % 8)
-        assert torch.equal(u[livet], scratch.view(p.blocks, p.unit_bytes)[livet]), f"layer {l}: live units"
+        assert bool((t.view(p.blocks, p.unit_bytes)[dead] == 0xA5).all()), f"layer {l}: a dead unit was written"
+    img[off[e] + byte] ^= mask
+
+    # the same through a pinned host image and the staging ring
+    pinned = torch.empty(m.image_bytes, dtype=torch.uint8, pin_memory=True)
+    blk_ps, blk_pr = z(m.num_blocks), z(m.num_blocks)
+    gms.restore(m, img, m.image_bytes)
+    gms.snapshot(m, pinned, m.image_bytes, gms.MEM_HOST_PINNED, blk_hash=blk_ps)
+    torch.cuda.synchronize()
+    assert np.array_equal(_u64(blk_ps), o_blk)
+    for lo in range(0, m.image_bytes, 1 << 30):  # the pinned image equals the (oracle-checked) device image
+        hi = min(m.image_bytes, lo + (1 << 30))
+        assert torch.equal(pinned[lo:hi].cuda(), img[lo:hi]), f"pinned image bytes {lo}..{hi}"
+    pinned[off[e] + byte] ^= mask
+    for t in pool:
+        t.fill_(0xA5)
+    gms.restore(m, pinned, m.image_bytes, gms.MEM_HOST_PINNED, expected=exp, blk_hash=blk_pr, mismatch_count=cnt,
+                mismatch_list=lst, mismatch_cap=8)
+    assert int(cnt.item()) == 1 and _u64(lst)[:1].tolist() == o_lst
+    assert np.array_equal(_u64(blk_pr), want)
+    del pinned
+    _free()
 
     # verify before reattach: a flipped bit in the pool itself
-    img[off[e] + bl * 4096 + bit // 8] ^= 1 << (bit % 8)
     gms.restore(m, img, m.image_bytes)
+    rng = np.random.default_rng(5)
     e2 = int(rng.integers(0, m.num_entries))
     b2 = int(rng.integers(0, p.unit_bytes))
     layer2, bid2 = e2 // p.n_live, int(live[e2 % p.n_live])
     pool[layer2][bid2 * p.unit_bytes + b2] ^= 0x80
     gms.verify(m, expected=exp, mismatch_count=cnt, mismatch_list=lst, mismatch_cap=8)
-    torch.cuda.synchronize()
-    assert int(cnt.item()) == 1 and int(lst[0].item()) == base[e2] + b2 // 4096
+    o_cnt2, o_lst2, _ = _oracle_flip(gen, sizes, base, o_blk, e2, b2, 0x80)
+    assert int(cnt.item()) == o_cnt2 == 1 and _u64(lst)[:1].tolist() == o_lst2
     m.close()
-    del pool, img, exp, scratch
+    del pool, img, exp, layer
     _free()
 
 
-def test_full_moe_shard_device():
-    """122 GB over 18,771 tensors; needs about 245 GB of HBM (allocations + image)."""
+@pytest.mark.timeout(1200)
+def test_full_moe_shard_device_and_host_image():
+    """122 GB over 18,771 tensors: the device-image leg needs about 245 GB of HBM
+    (allocations + image); the pageable-host leg then restores from 122 GB of host memory."""
     need_gpu()
     _free()
     free, _ = torch.cuda.mem_get_info()
     _, specs = synth.weight_set("moe")
     P = sum(sp.nbytes for sp in specs)
-    if free < 2 * P + (4 << 30):
+    if free < 2 * P + (8 << 30):
         pytest.skip(f"needs {2 * P / 1e9:.0f} GB free, have {free / 1e9:.0f} GB")
     seed, specs, ts = _alloc_or_skip(lambda: _weights("moe"))
     sizes = [sp.nbytes for sp in specs]
+    gen = _weight_gen(seed, sizes)
     m = gms.Manifest(ts, device=0)
     assert m.num_entries == 18_771 and m.payload_bytes == 122_143_121_408
-    off, base = m.layout()
+    z = lambda n: torch.zeros(n, dtype=torch.int64, device="cuda")  # noqa: E731
     img = _alloc_or_skip(lambda: torch.empty(m.image_bytes, dtype=torch.uint8, device="cuda"))
-    blk = torch.zeros(m.num_blocks, dtype=torch.int64, device="cuda")
-    gms.snapshot(m, img, m.image_bytes, blk_hash=blk)
-    torch.cuda.synchronize()
-    rng = np.random.default_rng(4)
-    hblk = to_u64(blk)
-    for i, b, g in _sampled_blocks(sizes, base, rng):
-        want = _host_block(seed, i, sizes[i], b)
-        got = img[off[i] + b * 4096: off[i] + b * 4096 + 4096].cpu().numpy()
-        assert np.array_equal(got[: want.size], want) and int(hblk[g]) == oracle.block_hash_at(want, sizes[i], b)
+    blk, ten, blk2 = z(m.num_blocks), z(m.num_entries), z(m.num_blocks)
+    cnt = torch.full((1,), 9, dtype=torch.int64, device="cuda")
+    gms.snapshot(m, img, m.image_bytes, blk_hash=blk, ten_hash=ten)
     for t in ts:
         t.view(torch.uint8).fill_(0xA5)
-    cnt = torch.full((1,), 9, dtype=torch.int64, device="cuda")
-    gms.restore(m, img, m.image_bytes, expected=blk, mismatch_count=cnt)
-    torch.cuda.synchronize()
+    gms.restore(m, img, m.image_bytes, expected=blk, blk_hash=blk2, mismatch_count=cnt)
     assert int(cnt.item()) == 0
+    h_blk, h_ten, h_blk2 = _u64(blk), _u64(ten), _u64(blk2)
     del img
     _free()
-    assert _equals_generated(ts, seed) == []
+    o_blk, _ = weight_parity(m, sizes, gen, {}, {"snapshot": h_blk, "restore": h_blk2}, {"snapshot": h_ten},
+                             restored=_restored(ts))
+
+    # the pageable host image: snapshot into ordinary host memory, poison, restore from it
+    host = np.empty(m.image_bytes, dtype=np.uint8)
+    blk_hs, blk_hr = z(m.num_blocks), z(m.num_blocks)
+    gms.snapshot_to_host(m, host, blk_hash=blk_hs)
+    for t in ts:
+        t.view(torch.uint8).fill_(0xA5)
+    gms.restore_from_host(m, host, expected=blk, blk_hash=blk_hr, mismatch_count=cnt)
+    assert int(cnt.item()) == 0
+    weight_parity(m, sizes, gen, {"host": host}, {"host snapshot": _u64(blk_hs), "host restore": _u64(blk_hr)}, {},
+                  restored=_restored(ts))
+    assert np.array_equal(h_blk, o_blk)
+    del host
     m.close()
-    del ts, blk
+    del ts, blk, blk2, blk_hs, blk_hr
     _free()
 
 

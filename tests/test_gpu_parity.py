@@ -174,8 +174,8 @@ def test_random_manifests(seed):
 
 
 def test_many_tiny_entries():
-    """200,000 entries of 1 to 300 bytes at every alignment: every block takes the byte-granular
-    path and most of each chunk's work units are empty."""
+    """200,000 entries of 1 to 300 bytes at every alignment: every block is a partial one (the
+    unaligned ones through the shifted path) and most of each chunk's work units are empty."""
     need_gpu()
     rng = np.random.default_rng(808)
     sizes = [int(v) for v in rng.integers(1, 301, 200_000)]
@@ -474,7 +474,8 @@ def test_mixed_manifest_takes_several_launch_groups(kind, staging):
         host[o:o + d.size] = d
     arena.buf.copy_(torch.from_numpy(host))
     m, _ = _round_trip(arena, datas, kind, staging=staging)
-    assert m.num_launch_groups == 2
+    # tiny and large chunks launch apart, and so do aligned and unaligned entries of a class
+    assert m.num_launch_groups >= 3
     # the host-image path over the same groups (it needs ring slots)
     m.set_staging(1 << 20, 2)
     o_img = oracle.pack(datas)
@@ -486,3 +487,65 @@ def test_mixed_manifest_takes_several_launch_groups(kind, staging):
     assert all(np.array_equal(a, b) for a, b in zip(back, datas)) and arena.outside_untouched(whole)
     assert to_u64(cnt)[0] == 0
     m.close()
+
+
+@pytest.mark.parametrize("kind,staging", [(gms.MEM_DEVICE, None), (gms.MEM_HOST_PINNED, (64 << 10, 2))],
+                         ids=["device", "ring_64k_x2"])
+def test_shifted_path_edges(kind, staging):
+    """Entries at every byte offset 1..15 from a 16-byte boundary, with sizes around the
+    granules a block shares with its neighbours (a block's last bytes short of, at and past the
+    next granule), single granules, several chunks and ragged tails: snapshot, restore and
+    verify equal the oracle and no byte outside an entry is written."""
+    need_gpu()
+    sizes, mis = [], []
+    for a in range(1, 16):
+        for n in (1, 15 - a, 16 - a, 17 - a, 4096 - a - 1, 4096 - a, 4096 - a + 1, 4096, 4097, 8192 - a,
+                  8192 + 16 - a, 2 * 65536 + 4096 - a, 65536 * 3 + 5, 300_001):
+            if n > 0:
+                sizes.append(n)
+                mis.append(a)
+    arena = Arena(sizes, misalign=mis, gap=40, seed=515)
+    datas = random_datas(sizes, seed=515)
+    arena.fill(datas)
+    m, _ = _round_trip(arena, datas, kind, staging=staging)
+    m.close()
+
+
+_ROUNDS_CHILD = r"""
+import sys
+sys.path[:0] = [sys.argv[1], sys.argv[1] + "/tests"]
+import numpy as np, torch
+import paper_2609_25451_amd as gms
+from gpu_util import Arena, random_datas
+import test_gpu_parity as t
+rng = np.random.default_rng(77)
+sizes = [int(v) for v in rng.integers(1, 200_000, 60)] + [3 << 20, 1 << 20] + [int(v) for v in rng.integers(1, 5000, 3000)]
+arena = Arena(sizes, misalign=lambda r: r.integers(0, 16) if r.random() < 0.3 else 0, gap=16, seed=77)
+datas = random_datas(sizes, seed=77)
+host = np.full(arena.total, 0xA5, dtype=np.uint8)
+for o, d in zip(arena.offsets, datas):
+    host[o:o + d.size] = d
+arena.buf.copy_(torch.from_numpy(host))
+m, _ = t._round_trip(arena, datas, gms.MEM_DEVICE)
+print("rounds ok", m.num_blocks, m.num_launch_groups, flush=True)
+"""
+
+
+@pytest.mark.parametrize("cap", [8, 64, 2048])
+def test_launches_loop_over_grid_rounds(cap):
+    """With the grid capped at `cap` workgroups (GMS_MAX_GRID, read once per process, so the
+    case runs in a child process), every launch loops over many grid-sized rounds: contiguous
+    and striped unit orders, paired and unit kernels, aligned and shifted entries; results
+    equal the oracle as with an uncapped grid."""
+    import os
+    import subprocess
+    import sys
+
+    need_gpu()
+    root = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+    env = dict(os.environ, GMS_MAX_GRID=str(cap))
+    print(f"child: GMS_MAX_GRID={cap}", flush=True)
+    r = subprocess.run([sys.executable, "-c", _ROUNDS_CHILD, root], env=env, capture_output=True, text=True,
+                       timeout=300)
+    assert r.returncode == 0, r.stdout[-2000:] + r.stderr[-4000:]
+    assert "rounds ok" in r.stdout
