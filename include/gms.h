@@ -215,6 +215,28 @@ int gms_verify(const gms_manifest *m, const uint64_t *expected_blk, uint64_t *bl
                uint64_t *ten_hash_out, uint64_t *mismatch_count_out, uint64_t *mismatch_list_out,
                uint64_t mismatch_cap, void *stream);
 
+/*
+ * For callers that cannot allocate (code under HIP graph capture, tight serving loops,
+ * harnesses that forbid hipMalloc): gms_restore from a pinned host image without any
+ * allocation.  gms_restore's staging ring is allocated on first use; here the staging area
+ * is a fixed device array of GMS_NOALLOC_STAGING_BYTES that the library holds on each
+ * device it runs on until the process ends, and every step runs on `stream`: each slice
+ * of the image (staging_bytes rounded down to whole chunks of the manifest; 0 = the whole
+ * area) is copied into the area by a kernel reading the pinned image over the host link,
+ * then scattered, hashed and compared by the kernels of gms_restore.  Arguments, outputs
+ * and results are those of gms_restore with image_kind GMS_MEM_HOST_PINNED; no hipMalloc,
+ * hipFree, stream or event is created, and only kernels are enqueued on `stream`.  The
+ * area is shared by every call on a device: calls that overlap on one device (different
+ * streams or threads) race, so a caller serializes them, for example on one stream.
+ * Errors: as gms_restore, plus GMS_ERR_SIZE for staging_bytes above
+ * GMS_NOALLOC_STAGING_BYTES or below the manifest's chunk size.
+ */
+#define GMS_NOALLOC_STAGING_BYTES (64ull << 20)
+int gms_restore_pinned_noalloc(const gms_manifest *m, const void *image, uint64_t image_bytes,
+                               uint64_t staging_bytes, const uint64_t *expected_blk, uint64_t *blk_hash_out,
+                               uint64_t *ten_hash_out, uint64_t *mismatch_count_out,
+                               uint64_t *mismatch_list_out, uint64_t mismatch_cap, void *stream);
+
 /* Flags of the image-file calls. */
 enum gms_file_flags {
     GMS_FILE_DIRECT = 1, /* O_DIRECT I/O (bypasses the page cache) when the file system and

@@ -86,6 +86,7 @@ _restore_file = _sig("gms_restore_from_file", INT,
 _snapshot_file = _sig("gms_snapshot_to_file", INT, [VP, ctypes.c_char_p, ctypes.c_uint32, ctypes.c_uint32, VP, VP, VP])
 _restore_host = _sig("gms_restore_from_host", INT, [VP, VP, U64, ctypes.c_uint32, VP, VP, VP, VP, VP, U64, VP])
 _snapshot_host = _sig("gms_snapshot_to_host", INT, [VP, VP, U64, ctypes.c_uint32, VP, VP, VP])
+_restore_noalloc = _sig("gms_restore_pinned_noalloc", INT, [VP, VP, U64, U64, VP, VP, VP, VP, VP, U64, VP])
 _pool_create = _sig("gms_pool_create", INT, [INT, U64, U64, ctypes.POINTER(VP)])
 _pool_destroy = _sig("gms_pool_destroy", None, [VP])
 _pool_alloc = _sig("gms_pool_alloc", INT, [VP, U64, U64, ctypes.POINTER(U64)])
@@ -340,6 +341,19 @@ def verify(m: Manifest, expected=None, blk_hash=None, ten_hash=None, mismatch_co
     _check(_verify(m._h, *h, mismatch_cap, _stream(stream)), "gms_verify")
 
 
+NOALLOC_STAGING_BYTES = 64 << 20  # GMS_NOALLOC_STAGING_BYTES
+
+
+def restore_pinned_noalloc(m: Manifest, image, image_bytes: int | None = None, staging_bytes: int = 0,
+                           expected=None, blk_hash=None, ten_hash=None, mismatch_count=None, mismatch_list=None,
+                           mismatch_cap: int = 0, stream=None) -> None:
+    """gms_restore from a pinned host image with no allocation (a fixed staging area)."""
+    img, nb = _image(image, image_bytes)
+    h = _hash_args(m, expected, blk_hash, ten_hash, mismatch_count, mismatch_list, mismatch_cap)
+    _check(_restore_noalloc(m._h, img, nb, staging_bytes, *h, mismatch_cap, _stream(stream)),
+           "gms_restore_pinned_noalloc")
+
+
 def restore_from_file(m: Manifest, path, file_offset: int = 0, flags: int = FILE_DIRECT, io_threads: int = 0,
                       expected=None, blk_hash=None, ten_hash=None, mismatch_count=None, mismatch_list=None,
                       mismatch_cap: int = 0, stream=None) -> None:
@@ -568,6 +582,7 @@ gms_restore = _restore
 gms_verify = _verify
 gms_layout = _layout
 gms_restore_from_file = _restore_file
+gms_restore_pinned_noalloc = _restore_noalloc
 gms_pool_create = _pool_create
 gms_pool_alloc = _pool_alloc
 gms_snapshot_to_file = _snapshot_file
