@@ -158,43 +158,45 @@ __device__ __forceinline__ u32x4 join(u32x4 lo, u32x4 hi, uint32_t o)
     }
 }
 
-__device__ __forceinline__ u32x4 shfl_up1(u32x4 v)  // lane l gets lane l - 1 (lane 0 its own)
+// Whole-wave rotations by one lane (DPP wave_ror:1 / wave_rol:1, a GFX9 feature):
+// ror gives lane l the value of lane l - 1 (lane 0 that of lane 63), rol the
+// value of lane l + 1 (lane 63 that of lane 0).
+template <int CTRL>
+__device__ __forceinline__ u32x4 rotate(u32x4 v)
 {
     u32x4 o;
-    o.x = (uint32_t)__shfl_up((int)v.x, 1, 64);
-    o.y = (uint32_t)__shfl_up((int)v.y, 1, 64);
-    o.z = (uint32_t)__shfl_up((int)v.z, 1, 64);
-    o.w = (uint32_t)__shfl_up((int)v.w, 1, 64);
+    o.x = (uint32_t)__builtin_amdgcn_mov_dpp((int)v.x, CTRL, 0xF, 0xF, false);
+    o.y = (uint32_t)__builtin_amdgcn_mov_dpp((int)v.y, CTRL, 0xF, 0xF, false);
+    o.z = (uint32_t)__builtin_amdgcn_mov_dpp((int)v.z, CTRL, 0xF, 0xF, false);
+    o.w = (uint32_t)__builtin_amdgcn_mov_dpp((int)v.w, CTRL, 0xF, 0xF, false);
     return o;
 }
+constexpr int kWaveRor1 = 0x13C;
+constexpr int kWaveRol1 = 0x134;
 
-__device__ __forceinline__ u32x4 shfl_down1(u32x4 v)  // lane l gets lane l + 1 (lane 63 its own)
+// Writes bytes [lo, hi) of v into the 16-byte-aligned granule p, in naturally
+// aligned pieces of 8, 4, 2 and 1 bytes.
+__device__ __forceinline__ void store_range(gbyte *p, u32x4 v, int lo, int hi)
 {
-    u32x4 o;
-    o.x = (uint32_t)__shfl_down((int)v.x, 1, 64);
-    o.y = (uint32_t)__shfl_down((int)v.y, 1, 64);
-    o.z = (uint32_t)__shfl_down((int)v.z, 1, 64);
-    o.w = (uint32_t)__shfl_down((int)v.w, 1, 64);
-    return o;
-}
-
-__device__ __forceinline__ u32x4 read_lane(u32x4 v, int l)
-{
-    u32x4 o;
-    o.x = (uint32_t)__builtin_amdgcn_readlane((int)v.x, l);
-    o.y = (uint32_t)__builtin_amdgcn_readlane((int)v.y, l);
-    o.z = (uint32_t)__builtin_amdgcn_readlane((int)v.z, l);
-    o.w = (uint32_t)__builtin_amdgcn_readlane((int)v.w, l);
-    return o;
-}
-
-// Writes bytes [lo, hi) of v into the 16-byte-aligned granule p, byte by byte.
-__device__ __forceinline__ void store_granule(gbyte *p, u32x4 v, int lo, int hi)
-{
+    const uint64_t w0 = (uint64_t)v.x | ((uint64_t)v.y << 32);
+    const uint64_t w1 = (uint64_t)v.z | ((uint64_t)v.w << 32);
 #pragma unroll 1
-    for (int q = lo; q < hi; ++q) {
-        const uint32_t d = q < 4 ? v.x : q < 8 ? v.y : q < 12 ? v.z : v.w;
-        p[q] = (uint8_t)(d >> (8 * (q & 3)));
+    for (int q = lo; q < hi;) {
+        const uint64_t w = q < 8 ? w0 : w1;
+        const int sh = 8 * (q & 7);
+        if ((q & 7) == 0 && q + 8 <= hi) {
+            *(__attribute__((address_space(1))) uint64_t *)(p + q) = w;
+            q += 8;
+        } else if ((q & 3) == 0 && q + 4 <= hi) {
+            *(__attribute__((address_space(1))) uint32_t *)(p + q) = (uint32_t)(w >> sh);
+            q += 4;
+        } else if ((q & 1) == 0 && q + 2 <= hi) {
+            *(__attribute__((address_space(1))) uint16_t *)(p + q) = (uint16_t)(w >> sh);
+            q += 2;
+        } else {
+            p[q] = (uint8_t)(w >> sh);
+            q += 1;
+        }
     }
 }
 
@@ -238,14 +240,18 @@ __device__ __forceinline__ void store_block(const u32x4 v[4], gbyte *p)
 // holds entry bytes [16s, 16s + 16) of the block and is hashed exactly as on
 // the aligned path.  The entry side is covered by aligned 16-byte granules:
 // granule s starts a bytes before segment s, so it takes the last a bytes of
-// segment s - 1 and the first 16 - a of segment s, which the wave moves
-// between neighbouring lanes (lane 0 takes lane 63 of the previous k).  A
-// restore stores every granule that lies inside the block with one 16-byte
-// store; only the two granules the block shares with its neighbours, and
-// those past the entry's end, are written byte by byte, so no byte outside
-// the entry is touched.  Snapshot and verify load the granules that hold a
-// byte of the block (whole granules never leave the entry's pages) and shift
-// the other way.  Returns the block hash (in lane 0).
+// segment s - 1 and the first 16 - a of segment s, which a whole-wave DPP
+// rotation brings from the neighbouring lane (lane 0 takes lane 63 of the
+// previous k).
+//  - A restore writes every granule with one 16-byte store.  The granule a
+//    block shares with the one before it is written by the later block, which
+//    also loads the earlier block's last image segment (same chunk, so the
+//    same image slot); only at a chunk's first and last byte, and at the
+//    entry's end, are granules written in part, with the widest aligned
+//    stores that fit, so no byte outside the entry is touched.
+//  - Snapshot and verify load the granules that hold a byte of the block
+//    (whole granules never leave the entry's pages) and rotate the other way.
+// Returns the block hash (in lane 0).
 template <int OP, bool HASH>
 __device__ __forceinline__ uint64_t move_block_shifted(const Chunk &c, uint32_t b, gbyte *img, uint64_t jg0,
                                                        uint64_t gblk, const HashOut &h, uint32_t lane, bool check)
@@ -254,64 +260,62 @@ __device__ __forceinline__ uint64_t move_block_shifted(const Chunk &c, uint32_t 
     const uint32_t bs = b * kBlockBytes;
     const int bv = (int)min(kBlockBytes, c.len - bs);            // real bytes of the block
     gbyte *const gran = (gbyte *)(c.addr - a) + bs + lane * 16;  // the lane's granule of k = 0
+    const u32x4 zero = {0u, 0u, 0u, 0u};
     u32x4 seg[4];
     if (OP == kRestore) {
 #pragma unroll
         for (int k = 0; k < 4; ++k) seg[k] = __builtin_nontemporal_load((const gvec *)(img + k * 1024));
-        // Whole granules are stored as they are formed.  The partial ones, at
-        // most two per block (the head, lane 0's granule 0, and the one holding
-        // the block's last byte), are kept and written once after the loop.
-        const u32x4 zero = {0u, 0u, 0u, 0u};
-        u32x4 head = zero, tail = zero;
-        int head_hi = 0, tail_hi = 0;
-        gbyte *tail_at = gran;
+        const bool inner = b > 0;  // the chunk's previous block shares granule 0
+        u32x4 before = zero;       // that block's last image segment, for lane 0
+        if (inner && lane == 0) before = *(const gvec *)(img - 16);
+        u32x4 r[4];
+#pragma unroll
+        for (int k = 0; k < 4; ++k) r[k] = rotate<kWaveRor1>(seg[k]);
+        // at most two partial granules per lane, written after the loop
+        u32x4 head = zero, part = zero;
+        int head_hi = 0, part_hi = 0;
+        gbyte *part_at = gran;
 #pragma unroll
         for (int k = 0; k < 4; ++k) {
-            u32x4 prev = shfl_up1(seg[k]);
-            if (k > 0) {
-                const u32x4 last = read_lane(seg[k - 1], 63);
-                if (lane == 0) prev = last;
-            }
+            const u32x4 prev = lane == 0 ? (k > 0 ? r[k - 1] : before) : r[k];
             const int s = 64 * k + (int)lane;
             const int hi = min(16, bv + (int)a - 16 * s);
             const u32x4 gv = join(prev, seg[k], 16 - a);
-            if (s == 0) {
+            if (s == 0 && !inner) {
                 head = gv;
                 head_hi = hi;
             } else if (hi >= 16) {
                 __builtin_nontemporal_store(gv, (gvec *)(gran + k * 1024));
             } else if (hi > 0) {
-                tail = gv;
-                tail_hi = hi;
-                tail_at = gran + k * 1024;
+                part = gv;
+                part_hi = hi;
+                part_at = gran + k * 1024;
             }
         }
-        if (lane == 63 && bv + (int)a > (int)kBlockBytes) {  // the granule shared with the next block
-            tail = join(seg[3], zero, 16 - a);
-            tail_hi = bv + (int)a - (int)kBlockBytes;
-            tail_at = gran + 3 * 1024 + 16;
+        // the granule after the block: the next block writes it, unless this is the chunk's last
+        const bool last = bs + kBlockBytes >= c.len;
+        if (last && lane == 63 && bv + (int)a > (int)kBlockBytes) {
+            part = join(seg[3], zero, 16 - a);
+            part_hi = bv + (int)a - (int)kBlockBytes;
+            part_at = gran + 3 * 1024 + 16;
         }
-        if (lane == 0) store_granule(gran, head, (int)a, head_hi);
-        if (tail_hi > 0) store_granule(tail_at, tail, 0, tail_hi);
+        if (lane == 0 && !inner) store_range(gran, head, (int)a, head_hi);
+        if (part_hi > 0) store_range(part_at, part, 0, part_hi);
     } else {
         u32x4 g[4];
-        const u32x4 zero = {0u, 0u, 0u, 0u};
 #pragma unroll
         for (int k = 0; k < 4; ++k) {
             const int s = 64 * k + (int)lane;
             g[k] = 16 * s < bv + (int)a ? __builtin_nontemporal_load((const gvec *)(gran + k * 1024)) : zero;
         }
-        u32x4 tail = zero;
+        u32x4 tail = zero;  // the granule after the block, for lane 63
         if (lane == 63 && bv + (int)a > (int)kBlockBytes) tail = *(const gvec *)(gran + 3 * 1024 + 16);
+        u32x4 n[4];
+#pragma unroll
+        for (int k = 0; k < 4; ++k) n[k] = rotate<kWaveRol1>(g[k]);
 #pragma unroll
         for (int k = 0; k < 4; ++k) {
-            u32x4 next = shfl_down1(g[k]);
-            if (k < 3) {
-                const u32x4 first = read_lane(g[k + 1], 0);
-                if (lane == 63) next = first;
-            } else if (lane == 63) {
-                next = tail;
-            }
+            const u32x4 next = lane == 63 ? (k < 3 ? n[k + 1] : tail) : n[k];
             const int s = 64 * k + (int)lane;
             const uint32_t valid = (uint32_t)max(0, min(16, bv - 16 * s));
             seg[k] = keep_bytes(join(g[k], next, a), valid);
