@@ -408,8 +408,8 @@ int gms_pool_mapping_of(const gms_pool *p, uint64_t addr, uint64_t *map_addr, ui
  * from an image) and commit again, which makes it valid.
  *
  * In one process the store's pool is the engine's own mapping of the
- * allocations; the paper's cross-process export of allocation handles is not
- * part of this library.  A store made with device GMS_HOST_ONLY runs the
+ * allocations; gms_owner_* and gms_client_* below run the same protocol across
+ * processes.  A store made with device GMS_HOST_ONLY runs the
  * protocol alone, without memory (no allocations; commit takes no entries).
  * Store calls are thread-safe and synchronous: each returns after the device
  * work it enqueues on `stream` has finished.  Leases are non-zero ids, valid
@@ -489,6 +489,83 @@ int gms_store_disconnect(gms_store *s, uint64_t lease);
  * block); NULL while nothing is committed.  Valid until the next writer connects. */
 const gms_manifest *gms_store_layout(const gms_store *s);
 const uint64_t *gms_store_block_hashes(const gms_store *s);
+
+/*
+ * The model-state store across processes (paper section 3.2, GMS and Figure 4; section 4:
+ * a GMS process per GPU owns the allocations and exports them as POSIX file descriptors over
+ * a Unix-domain socket, so that an engine's crash cannot take them with it).
+ *
+ * Owner.  gms_owner_create binds a Unix-domain socket at `socket_path` (an existing socket
+ * file there is replaced) for `device`; gms_owner_run serves clients until gms_owner_stop
+ * (callable from any thread); gms_owner_destroy releases every allocation and removes the
+ * socket file.  The owner creates device memory with HIP virtual memory and never maps it;
+ * each allocation (at most GMS_IPC_PIECE_BYTES) travels as one dma-buf descriptor.  It runs
+ * the states and transitions of the in-process store above: one writer, then COMMITTED;
+ * readers; a writer's connection that closes before commit (disconnect, abort or the
+ * process's death) discards every allocation (EMPTY); a reader's connection that closes
+ * ends only its lease.  An owner made with device GMS_HOST_ONLY runs the protocol alone,
+ * without memory.
+ *
+ * Clients.  gms_client_connect opens a lease: GMS_LEASE_RW (exclusive; from EMPTY, or from
+ * COMMITTED reusing the allocation set) or GMS_LEASE_RO (on committed state).  The client
+ * maps every allocation as external memory (hipImportExternalMemory of the descriptor):
+ * on this ROCm a virtual-memory handle cannot be imported by a process other than its
+ * exporter, so the mappings carry no access flags; a reader's read-only use is this
+ * library's contract (nothing here writes through a reader's mapping) and readers verify
+ * the state before they use it.  A writer takes memory with gms_client_alloc (first fit in
+ * slabs of GMS_IPC_PIECE_BYTES; a request above half a slab gets an allocation of its own;
+ * GMS_ERR_SIZE above GMS_IPC_PIECE_BYTES), populates it, and commits entries (each inside
+ * one of its allocations): the library hashes every 4 KiB block of them (and compares with
+ * expected_blk when given, refusing the commit on a mismatch with GMS_ERR_INTEGRITY while
+ * the writer keeps its lease), synchronizes the device, and the owner records the layout
+ * and the hashes; the write lease ends (the writer must not write after it).  A client's
+ * layout is the committed entries at its own addresses (gms_client_layout,
+ * gms_client_manifest for gms_restore / gms_verify; empty before the first commit): a
+ * reader's to use, a writer's to repopulate.  With GMS_CONNECT_VERIFY a reader re-hashes
+ * the layout against the commit-time hashes before the lease is granted, and any mismatch
+ * refuses the lease (GMS_ERR_INTEGRITY, the count in *mismatch_count_out) and invalidates
+ * the committed state at the owner until a writer commits again.  gms_client_verify
+ * re-hashes later (a mismatch invalidates the state; the reader keeps its lease).
+ * gms_client_disconnect unmaps everything and ends the lease.  Client calls are
+ * synchronous and not thread-safe on one client object.
+ * Errors: GMS_ERR_IO (socket), GMS_ERR_STATE (lease protocol), GMS_ERR_INTEGRITY,
+ * GMS_ERR_INVALID, GMS_ERR_SIZE, GMS_ERR_NOMEM, GMS_ERR_HIP.
+ */
+#define GMS_IPC_PIECE_BYTES (1ull << 30)
+
+enum gms_lease_mode {
+    GMS_LEASE_RW = 1,
+    GMS_LEASE_RO = 2
+};
+
+typedef struct gms_owner gms_owner;
+typedef struct gms_client gms_client;
+
+int gms_owner_create(const char *socket_path, int device, gms_owner **out);
+int gms_owner_run(gms_owner *o);
+void gms_owner_stop(gms_owner *o);
+/* State (enum gms_store_state), reader count, invalid flag and live allocations; outputs may
+ * be NULL.  gms_owner_query asks a running owner the same over its socket. */
+int gms_owner_status(gms_owner *o, int *state, uint32_t *readers, int *invalid, uint64_t *allocations);
+int gms_owner_query(const char *socket_path, int *state, uint32_t *readers, int *invalid, uint64_t *allocations);
+void gms_owner_destroy(gms_owner *o);
+
+int gms_client_connect(const char *socket_path, int mode, uint32_t flags, void *stream, gms_client **out,
+                       uint64_t *mismatch_count_out);
+/* The lease id (0 once it ended) and the owner's device; outputs may be NULL. */
+int gms_client_lease(const gms_client *c, uint64_t *lease_out, int *device_out);
+int gms_client_alloc(gms_client *c, uint64_t bytes, uint64_t align, uint64_t *addr_out);
+int gms_client_free(gms_client *c, uint64_t addr);
+int gms_client_commit(gms_client *c, const gms_entry *entries, uint64_t n, const uint64_t *expected_blk,
+                      uint64_t *mismatch_count_out, void *stream);
+int gms_client_abort(gms_client *c);
+/* Reader: the committed entries at this process's addresses (up to cap; *n_out the count). */
+int gms_client_layout(const gms_client *c, gms_entry *entries_out, uint64_t cap, uint64_t *n_out);
+const gms_manifest *gms_client_manifest(const gms_client *c);
+const uint64_t *gms_client_block_hashes(const gms_client *c);
+int gms_client_verify(gms_client *c, uint64_t *mismatch_count_out, uint64_t *mismatch_list_out, uint64_t cap,
+                      void *stream);
+int gms_client_disconnect(gms_client *c);
 
 /* Static description of a status code. */
 const char *gms_status_str(int status);

@@ -110,6 +110,24 @@ _store_verify = _sig("gms_store_verify", INT, [VP, ctypes.POINTER(U64), VP, U64,
 _store_disconnect = _sig("gms_store_disconnect", INT, [VP, U64])
 _store_layout = _sig("gms_store_layout", VP, [VP])
 _store_block_hashes = _sig("gms_store_block_hashes", VP, [VP])
+_owner_create = _sig("gms_owner_create", INT, [ctypes.c_char_p, INT, ctypes.POINTER(VP)])
+_owner_run = _sig("gms_owner_run", INT, [VP])
+_owner_stop = _sig("gms_owner_stop", None, [VP])
+_owner_status = _sig("gms_owner_status", INT, [VP, VP, VP, VP, VP])
+_owner_query = _sig("gms_owner_query", INT, [ctypes.c_char_p, VP, VP, VP, VP])
+_owner_destroy = _sig("gms_owner_destroy", None, [VP])
+_client_connect = _sig("gms_client_connect", INT,
+                       [ctypes.c_char_p, INT, ctypes.c_uint32, VP, ctypes.POINTER(VP), ctypes.POINTER(U64)])
+_client_lease = _sig("gms_client_lease", INT, [VP, VP, VP])
+_client_alloc = _sig("gms_client_alloc", INT, [VP, U64, U64, ctypes.POINTER(U64)])
+_client_free = _sig("gms_client_free", INT, [VP, U64])
+_client_commit = _sig("gms_client_commit", INT, [VP, ctypes.POINTER(GmsEntry), U64, VP, ctypes.POINTER(U64), VP])
+_client_abort = _sig("gms_client_abort", INT, [VP])
+_client_layout = _sig("gms_client_layout", INT, [VP, VP, U64, ctypes.POINTER(U64)])
+_client_manifest = _sig("gms_client_manifest", VP, [VP])
+_client_block_hashes = _sig("gms_client_block_hashes", VP, [VP])
+_client_verify = _sig("gms_client_verify", INT, [VP, ctypes.POINTER(U64), VP, U64, VP])
+_client_disconnect = _sig("gms_client_disconnect", INT, [VP])
 _status_str = _sig("gms_status_str", ctypes.c_char_p, [INT])
 _last_error = _sig("gms_last_error", ctypes.c_char_p, [])
 _abi = _sig("gms_abi_version", INT, [])
@@ -570,6 +588,120 @@ class ReadLease(_Lease):
     """Read-only lease on committed state."""
 
 
+LEASE_RW = 1
+LEASE_RO = 2
+IPC_PIECE_BYTES = 1 << 30  # GMS_IPC_PIECE_BYTES
+
+
+def owner_query(socket_path) -> tuple:
+    """(state name, readers, invalid, allocations) of a running owner, over its socket."""
+    st, rd, inv, al = INT(), ctypes.c_uint32(), INT(), U64()
+    _check(_owner_query(os.fsencode(socket_path), ctypes.byref(st), ctypes.byref(rd), ctypes.byref(inv),
+                        ctypes.byref(al)), "gms_owner_query")
+    return STORE_STATES[st.value], int(rd.value), bool(inv.value), int(al.value)
+
+
+class Owner:
+    """The GMS owner of one device's model-state allocations (see gms_owner_* in include/gms.h).
+    ``run()`` serves until ``stop()``; it releases the interpreter lock while it runs."""
+
+    def __init__(self, socket_path, device: int = 0):
+        h = VP()
+        _check(_owner_create(os.fsencode(socket_path), device, ctypes.byref(h)), "gms_owner_create")
+        self._h = h
+        self.path = os.fspath(socket_path)
+
+    def run(self) -> None:
+        _check(_owner_run(self._h), "gms_owner_run")
+
+    def stop(self) -> None:
+        if self._h.value:
+            _owner_stop(self._h)
+
+    def status(self) -> tuple:
+        st, rd, inv, al = INT(), ctypes.c_uint32(), INT(), U64()
+        _check(_owner_status(self._h, ctypes.byref(st), ctypes.byref(rd), ctypes.byref(inv), ctypes.byref(al)),
+               "gms_owner_status")
+        return STORE_STATES[st.value], int(rd.value), bool(inv.value), int(al.value)
+
+    def close(self) -> None:
+        if getattr(self, "_h", None) is not None and self._h.value:
+            _owner_destroy(self._h)
+            self._h = VP()
+
+
+class Client:
+    """A lease on an owner's model state from this process (see gms_client_* in include/gms.h)."""
+
+    def __init__(self, socket_path, mode: int, verify: bool = False, stream=None):
+        h, cnt = VP(), U64()
+        rc = _client_connect(os.fsencode(socket_path), mode, CONNECT_VERIFY if verify else 0, _stream(stream),
+                             ctypes.byref(h), ctypes.byref(cnt))
+        if rc != GMS_OK:
+            raise GmsError(rc, "gms_client_connect", int(cnt.value))
+        self._h = h
+        self.mode = mode
+
+    def info(self) -> dict:
+        lease, dev = U64(), INT()
+        _check(_client_lease(self._h, ctypes.byref(lease), ctypes.byref(dev)), "gms_client_lease")
+        return {"lease": int(lease.value), "device": int(dev.value)}
+
+    def alloc(self, nbytes: int, align: int = 0) -> int:
+        out = U64()
+        _check(_client_alloc(self._h, nbytes, align, ctypes.byref(out)), "gms_client_alloc")
+        return int(out.value)
+
+    def free(self, addr: int) -> None:
+        _check(_client_free(self._h, addr), "gms_client_free")
+
+    def commit(self, entries, expected=None, stream=None) -> None:
+        ranges = _ranges(entries)
+        nb = sum(-(-b // BLOCK_BYTES) for _, b in ranges)
+        cnt = U64()
+        rc = _client_commit(self._h, _entry_array(ranges), len(ranges), _buf(expected, nb * 8, "expected", True),
+                            ctypes.byref(cnt), _stream(stream))
+        if rc != GMS_OK:
+            raise GmsError(rc, "gms_client_commit", int(cnt.value))
+
+    def abort(self) -> None:
+        _check(_client_abort(self._h), "gms_client_abort")
+
+    def layout(self) -> list:
+        n = U64()
+        _check(_client_layout(self._h, None, 0, ctypes.byref(n)), "gms_client_layout")
+        arr = (GmsEntry * max(int(n.value), 1))()
+        _check(_client_layout(self._h, arr, int(n.value), ctypes.byref(n)), "gms_client_layout")
+        return [(int(e.addr), int(e.nbytes)) for e in arr[:int(n.value)]]
+
+    def manifest(self) -> Manifest | None:
+        """The committed layout as a manifest owned by the client (valid until disconnect)."""
+        h = _client_manifest(self._h)
+        return Manifest._borrow(h, self) if h else None
+
+    def block_hashes_ptr(self) -> int:
+        return int(_client_block_hashes(self._h) or 0)
+
+    def verify(self, mismatch_list=None, mismatch_cap: int = 0, stream=None) -> int:
+        cnt = U64()
+        m = _client_manifest(self._h)
+        nb = int(_num_blocks(m)) if m else 0
+        lst = _buf(mismatch_list, min(int(mismatch_cap), nb) * 8, "mismatch_list", True)
+        _check(_client_verify(self._h, ctypes.byref(cnt), lst, mismatch_cap, _stream(stream)), "gms_client_verify")
+        return int(cnt.value)
+
+    def close(self) -> None:
+        if getattr(self, "_h", None) is not None and self._h.value:
+            h, self._h = self._h, VP()
+            _check(_client_disconnect(h), "gms_client_disconnect")
+
+    def __enter__(self):
+        return self
+
+    def __exit__(self, *exc):
+        self.close()
+
+
 def status_str(rc: int) -> str:
     return _status_str(rc).decode()
 
@@ -600,3 +732,10 @@ gms_store_commit = _store_commit
 gms_store_abort = _store_abort
 gms_store_disconnect = _store_disconnect
 gms_store_verify = _store_verify
+gms_owner_create = _owner_create
+gms_owner_run = _owner_run
+gms_owner_stop = _owner_stop
+gms_owner_query = _owner_query
+gms_client_connect = _client_connect
+gms_client_commit = _client_commit
+gms_client_disconnect = _client_disconnect

@@ -483,6 +483,14 @@ int gms_manifest_create(const gms_entry *entries, uint64_t n, int device, uint64
                         gms_manifest **out)
 {
     gms::clear_error();
+    return gms::manifest_create(entries, n, device, chunk_bytes, true, out);
+}
+
+}  // extern "C"
+
+int gms::manifest_create(const gms_entry *entries, uint64_t n, int device, uint64_t chunk_bytes, bool check_ranges,
+                         gms_manifest **out)
+{
     if (!out) return fail(GMS_ERR_INVALID, "out is null");
     *out = nullptr;
     if (n && !entries) return fail(GMS_ERR_INVALID, "entries is null");
@@ -520,6 +528,7 @@ int gms_manifest_create(const gms_entry *entries, uint64_t n, int device, uint64
         // reusing the previous allocation's bounds)
         uint64_t cur_lo = 0, cur_hi = 0;
         for (uint64_t i : order) {
+            if (!check_ranges) break;
             const gms_entry &r = entries[i];
             if (r.addr >= cur_lo && r.addr + r.nbytes <= cur_hi) continue;
             char what[48];
@@ -597,6 +606,8 @@ int gms_manifest_create(const gms_entry *entries, uint64_t n, int device, uint64
     *out = m;
     return GMS_OK;
 }
+
+extern "C" {
 
 void gms_manifest_destroy(gms_manifest *m)
 {

@@ -128,6 +128,11 @@ int pool_set_access_all(gms_pool *p, bool read_only);
 bool pool_holds(gms_pool *p, uint64_t addr, uint64_t bytes);
 int pool_device(const gms_pool *p);
 
+// gms_manifest_create; with check_ranges false the ranges are not checked
+// against the runtime's allocations (for mappings the runtime does not report
+// whole, such as imported external memory, which the caller has checked).
+int manifest_create(const gms_entry *entries, uint64_t n, int device, uint64_t chunk_bytes, bool check_ranges,
+                    gms_manifest **out);
 void free_ring(gms_manifest *m);
 int ensure_ring(gms_manifest *m);       // device slots, copy stream, events, slice table
 int ensure_host_ring(gms_manifest *m);  // plus pinned host slots
