@@ -574,7 +574,8 @@ const char *gms_status_str(int status);
 const char *gms_last_error(void);
 
 /* ABI version of this header (2: adds the model-state store and GMS_ERR_INTEGRITY;
- * 3: adds gms_restore_from_host and gms_snapshot_to_host). */
+ * 3: adds gms_restore_from_host and gms_snapshot_to_host; 4: adds gms_restore_pinned_noalloc,
+ * the owner process and its clients). */
 int gms_abi_version(void);
 
 #ifdef __cplusplus

@@ -459,7 +459,7 @@ using gms::make_hash;
 
 extern "C" {
 
-int gms_abi_version(void) { return 3; }
+int gms_abi_version(void) { return 4; }
 
 const char *gms_status_str(int status)
 {

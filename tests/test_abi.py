@@ -22,7 +22,7 @@ def test_exports_every_declared_symbol():
     exported = {line.split()[-1] for line in out.splitlines() if line.strip()}
     missing = [s for s in declared if s not in exported]
     assert not missing, f"declared but not exported: {missing}"
-    assert gms.abi_version() == 3
+    assert gms.abi_version() == 4
 
 
 def _host_manifest(sizes, base=1 << 40, gap=0, chunk_bytes=0, align=1):
