@@ -31,7 +31,7 @@ sys.path.insert(0, ROOT)
 METRIC = "restore+verify GB/s on 1 GPU; seconds to restore a 16 GB weight shard"
 HBM_PEAK_GBS = 8000.0
 ALL_ROWS = ["main", "snapshot", "plain", "verify", "sequential", "unaligned", "tiny", "mixed", "h2d", "file", "kv",
-            "kv_vmm", "store", "recovery", "copy", "cpu", "shards"]
+            "kv_vmm", "store", "owner", "recovery", "copy", "cpu", "shards"]
 # What shapes the measured kernel's accesses: the kernel and its launch code, the
 # header's block and default chunk sizes and the chunking in manifest creation.
 KERNEL_SOURCES = ["paper_2609_25451_amd/csrc/gms_kernels.hip", "paper_2609_25451_amd/csrc/gms_internal.h"]
@@ -348,6 +348,13 @@ def main():
         th = statistics.median(timer.run(h2d, 3))
         link_after = link_now(torch, timer)
         assert int(hc.item()) == 0
+
+        def h2d_noalloc():  # the same restore with no allocation: fixed staging area, one stream
+            gms.restore_pinned_noalloc(m, pinned, m.image_bytes, expected=expected, mismatch_count=hc)
+
+        h2d_noalloc()
+        tna = statistics.median(timer.run(h2d_noalloc, 3))
+        assert int(hc.item()) == 0
         m.set_staging(0, 0)
         tz = statistics.median(timer.run(h2d, 2))
         assert int(hc.item()) == 0
@@ -360,6 +367,8 @@ def main():
             "restore_untimed_calls_s": h2d_warm, "link_right_after_GB_s": link_after,
             "link_frac": P / th / 1e9 / link,
             "restore_verify_zero_copy_s": tz, "restore_verify_zero_copy_GB_s": P / tz / 1e9,
+            "restore_verify_noalloc_s": tna, "restore_verify_noalloc_GB_s": P / tna / 1e9,
+            "noalloc_link_frac": P / tna / 1e9 / link,
             "link_peak_d2h_GB_s": link_d2h,
             "snapshot_to_pinned_s": snap_h, "snapshot_to_pinned_GB_s": P / snap_h / 1e9,
             "snapshot_link_frac": P / snap_h / 1e9 / link_d2h,
@@ -379,6 +388,8 @@ def main():
         result_rows["kv_pool_vmm"] = bench_kv_vmm(torch, np, gms, synth, timer)
     if "store" in rows:
         result_rows["store"] = bench_store(torch, gms, m, image, expected)
+    if "owner" in rows:
+        result_rows["owner"] = bench_owner(torch, gms, timer, m, image, expected)
     if "recovery" in rows:
         result_rows["recovery"] = bench_recovery(torch, np, gms, synth, m, image, expected)
 
@@ -900,6 +911,69 @@ def bench_store(torch, gms, m, image, expected):
         return out
     finally:
         store.close()
+
+
+def bench_owner(torch, gms, timer, m, image, expected):
+    """The lease protocol across processes on the llama8b set: an owner process holds the
+    allocations; this process, as the writer, populates them from the device image with a fused
+    restore+verify and commits; then, as a replacement engine, attaches read-only after
+    re-hashing all of it.  Wall times of the synchronous calls; the restore and the re-verify
+    are also timed as kernels on the owner's memory (mapped here as external memory)."""
+    import signal
+    import subprocess
+    import tempfile
+
+    sizes = list(m.sizes)
+    P, nb = m.payload_bytes, m.num_blocks
+    sock = os.path.join(tempfile.mkdtemp(prefix="gms-"), "owner.sock")
+    t0 = time.perf_counter()
+    p = subprocess.Popen([sys.executable, "-m", "paper_2609_25451_amd.owner", sock, "--device", "0"], cwd=ROOT,
+                         stdout=subprocess.PIPE, stderr=subprocess.PIPE, text=True)
+    try:
+        line = p.stdout.readline()
+        assert line.startswith("owner ready"), line + p.stderr.read()
+        start = time.perf_counter() - t0
+        cnt = torch.zeros(1, dtype=torch.int64, device="cuda")
+        t0 = time.perf_counter()
+        w = gms.Client(sock, gms.LEASE_RW)
+        addrs = [w.alloc(n) for n in sizes]
+        alloc = time.perf_counter() - t0
+        entries = list(zip(addrs, sizes))
+        wm = w.manifest_over(entries)
+        tr = settled(timer, lambda: gms.restore(wm, image, expected=expected, mismatch_count=cnt), warm=2, reps=5)
+        assert int(cnt.item()) == 0
+        wm.close()
+        t0 = time.perf_counter()
+        w.commit(entries, expected=expected)
+        commit = time.perf_counter() - t0
+        w.close()
+        attach = []
+        for _ in range(3):
+            t0 = time.perf_counter()
+            r = gms.Client(sock, gms.LEASE_RO, verify=True)
+            attach.append(time.perf_counter() - t0)
+            rm = r.manifest()
+            tv = settled(timer, lambda: gms.verify(rm, expected=expected, mismatch_count=cnt), warm=2, reps=5)
+            assert int(cnt.item()) == 0
+            r.close()
+        state, readers, invalid, allocs = gms.owner_query(sock)
+        assert (state, readers, invalid) == ("COMMITTED", 0, False)
+        out = {"payload_bytes": P, "owner_start_s": start, "allocations": allocs, "writer_alloc_s": alloc,
+               "populate_restore_verify_s": tr, "populate_hbm_frac": (2 * P + 8 * nb) / tr / 1e9 / HBM_PEAK_GBS,
+               "commit_s": commit, "attach_ro_verified_s": statistics.median(attach),
+               "attach_runs_s": [round(a, 4) for a in attach], "reverify_s": tv,
+               "reverify_hbm_frac": (P + 8 * nb) / tv / 1e9 / HBM_PEAK_GBS}
+        log(f"owner process: {allocs} allocations, populate {tr * 1e3:.2f} ms "
+            f"({out['populate_hbm_frac'] * 100:.1f}% of HBM peak), commit {commit * 1e3:.1f} ms, "
+            f"verified attach from another lease {out['attach_ro_verified_s'] * 1e3:.1f} ms")
+        return out
+    finally:
+        p.send_signal(signal.SIGTERM)
+        try:
+            p.wait(timeout=60)
+        except subprocess.TimeoutExpired:
+            p.kill()
+            p.wait()
 
 
 def bench_recovery(torch, np, gms, synth, m, image, expected):

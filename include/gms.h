@@ -562,6 +562,12 @@ int gms_client_abort(gms_client *c);
 /* Reader: the committed entries at this process's addresses (up to cap; *n_out the count). */
 int gms_client_layout(const gms_client *c, gms_entry *entries_out, uint64_t cap, uint64_t *n_out);
 const gms_manifest *gms_client_manifest(const gms_client *c);
+/* A manifest over entries inside this client's allocations (gms_manifest_create's arguments and
+ * errors; the caller destroys it), for gms_restore into a writer's memory before its first
+ * commit, or any other data-plane call on client memory: the runtime does not report the extent
+ * of these mappings, so gms_manifest_create cannot check them. */
+int gms_client_manifest_create(const gms_client *c, const gms_entry *entries, uint64_t n, uint64_t chunk_bytes,
+                               gms_manifest **out);
 const uint64_t *gms_client_block_hashes(const gms_client *c);
 int gms_client_verify(gms_client *c, uint64_t *mismatch_count_out, uint64_t *mismatch_list_out, uint64_t cap,
                       void *stream);

@@ -125,6 +125,8 @@ _client_commit = _sig("gms_client_commit", INT, [VP, ctypes.POINTER(GmsEntry), U
 _client_abort = _sig("gms_client_abort", INT, [VP])
 _client_layout = _sig("gms_client_layout", INT, [VP, VP, U64, ctypes.POINTER(U64)])
 _client_manifest = _sig("gms_client_manifest", VP, [VP])
+_client_manifest_create = _sig("gms_client_manifest_create", INT, [VP, ctypes.POINTER(GmsEntry), U64, U64,
+                                                                   ctypes.POINTER(VP)])
 _client_block_hashes = _sig("gms_client_block_hashes", VP, [VP])
 _client_verify = _sig("gms_client_verify", INT, [VP, ctypes.POINTER(U64), VP, U64, VP])
 _client_disconnect = _sig("gms_client_disconnect", INT, [VP])
@@ -681,6 +683,18 @@ class Client:
 
     def block_hashes_ptr(self) -> int:
         return int(_client_block_hashes(self._h) or 0)
+
+    def manifest_over(self, entries, chunk_bytes: int = 0) -> Manifest:
+        """A manifest (owned by the caller) over entries inside this client's allocations."""
+        ranges = _ranges(entries)
+        h = VP()
+        _check(_client_manifest_create(self._h, _entry_array(ranges), len(ranges), chunk_bytes, ctypes.byref(h)),
+               "gms_client_manifest_create")
+        m = Manifest.__new__(Manifest)
+        m._h = h
+        m._owned = True
+        m.sizes = [b for _, b in ranges]
+        return m
 
     def verify(self, mismatch_list=None, mismatch_cap: int = 0, stream=None) -> int:
         cnt = U64()

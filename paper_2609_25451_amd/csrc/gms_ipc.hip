@@ -62,7 +62,7 @@ namespace {
 
 constexpr uint32_t kMagic = 0x31534D47u;  // "GMS1"
 constexpr uint32_t kMaxFdsPerMsg = 128;
-constexpr uint64_t kMaxPayload = 1ull << 34;  // refuse absurd lengths from a broken peer
+constexpr uint64_t kMaxPayload = 1ull << 32;  // refuse absurd lengths from a broken peer
 
 enum Op : uint32_t {
     kHelloRW = 1,
@@ -1126,6 +1126,32 @@ int gms_client_layout(const gms_client *c, gms_entry *entries_out, uint64_t cap,
 }
 
 const gms_manifest *gms_client_manifest(const gms_client *c) { return c ? c->m : nullptr; }
+
+int gms_client_manifest_create(const gms_client *c, const gms_entry *entries, uint64_t n, uint64_t chunk_bytes,
+                               gms_manifest **out)
+{
+    gms::clear_error();
+    if (!c || !out) return fail(GMS_ERR_INVALID, "client or out is null");
+    *out = nullptr;
+    if (n && !entries) return fail(GMS_ERR_INVALID, "entries is null");
+    if (c->device == GMS_HOST_ONLY) return fail(GMS_ERR_STATE, "the owner has no device memory");
+    for (uint64_t i = 0; i < n; ++i) {
+        const gms_entry &e = entries[i];
+        if (!e.nbytes) continue;
+        bool inside = false;
+        for (const auto &kv : c->allocs) {
+            const ClientAlloc &a = kv.second;
+            if (e.addr >= a.va && e.addr + e.nbytes >= e.addr && e.addr + e.nbytes <= a.va + a.bytes) {
+                inside = true;
+                break;
+            }
+        }
+        if (!inside)
+            return fail(GMS_ERR_INVALID, "entry %llu [%#llx, +%llu) is not inside one allocation of this client",
+                        (unsigned long long)i, (unsigned long long)e.addr, (unsigned long long)e.nbytes);
+    }
+    return gms::manifest_create(entries, n, c->device, chunk_bytes, false, out);
+}
 
 const uint64_t *gms_client_block_hashes(const gms_client *c) { return c ? c->d_hash : nullptr; }
 
