@@ -262,6 +262,58 @@ __device__ __forceinline__ uint64_t move_block_shifted(const Chunk &c, uint32_t 
     gbyte *const gran = (gbyte *)(c.addr - a) + bs + lane * 16;  // the lane's granule of k = 0
     const u32x4 zero = {0u, 0u, 0u, 0u};
     u32x4 seg[4];
+
+    // Interior blocks, most of any entry, skip the per-segment bounds below: for a
+    // restore, a full block that is not the chunk's last writes whole granules
+    // only (bar a chunk's first granule) and leaves the granule after it to the
+    // next block; snapshot and verify of any full block load every granule and
+    // the one after it, which holds the block's last a bytes.
+    const bool interior = OP == kRestore ? bs + kBlockBytes < c.len : bs + kBlockBytes <= c.len;
+    if (interior) {
+        if (OP == kRestore) {
+#pragma unroll
+            for (int k = 0; k < 4; ++k) seg[k] = __builtin_nontemporal_load((const gvec *)(img + k * 1024));
+            const bool inner = b > 0;
+            u32x4 before = zero;
+            if (inner && lane == 0) before = *(const gvec *)(img - 16);
+            u32x4 r[4];
+#pragma unroll
+            for (int k = 0; k < 4; ++k) r[k] = rotate<kWaveRor1>(seg[k]);
+#pragma unroll
+            for (int k = 0; k < 4; ++k) {
+                const u32x4 prev = lane == 0 ? (k > 0 ? r[k - 1] : before) : r[k];
+                const u32x4 gv = join(prev, seg[k], 16 - a);
+                if (k == 0 && !inner && lane == 0)
+                    store_range(gran, gv, (int)a, 16);
+                else
+                    __builtin_nontemporal_store(gv, (gvec *)(gran + k * 1024));
+            }
+        } else {
+            u32x4 g[4];
+#pragma unroll
+            for (int k = 0; k < 4; ++k) g[k] = __builtin_nontemporal_load((const gvec *)(gran + k * 1024));
+            u32x4 tail = zero;
+            if (lane == 63) tail = *(const gvec *)(gran + 3 * 1024 + 16);
+            u32x4 n[4];
+#pragma unroll
+            for (int k = 0; k < 4; ++k) n[k] = rotate<kWaveRol1>(g[k]);
+#pragma unroll
+            for (int k = 0; k < 4; ++k) {
+                const u32x4 next = lane == 63 ? (k < 3 ? n[k + 1] : tail) : n[k];
+                seg[k] = join(g[k], next, a);
+                if (OP == kSnapshot) __builtin_nontemporal_store(seg[k], (gvec *)(img + k * 1024));
+            }
+        }
+        uint64_t tacc = 0;
+        if (HASH) {
+            uint64_t hl = 0;
+#pragma unroll
+            for (int k = 0; k < 4; ++k) hl ^= seg_hash(seg[k], jg0 + (uint64_t)k * kSegStrideG);
+            tacc = finish_block(hl, gblk, h, lane, check, check ? h.expected[gblk] : 0);
+        }
+        return tacc;
+    }
+
     if (OP == kRestore) {
 #pragma unroll
         for (int k = 0; k < 4; ++k) seg[k] = __builtin_nontemporal_load((const gvec *)(img + k * 1024));
