@@ -454,8 +454,8 @@ int gms_store_free(gms_store *s, uint64_t lease, uint64_t addr);
 
 /*
  * Writer only: commits entries[0..n) (each inside one allocation of the store) as the
- * layout, hashes its blocks, synchronizes the device (so device work of the writer on any
- * stream has finished) and maps the pool read-only; the lease ends.  With
+ * layout: synchronizes the device (so device work of the writer on any stream has
+ * finished), hashes the layout's blocks and maps the pool read-only; the lease ends.  With
  * expected_blk (device, one u64 per block of the layout, as gms_snapshot writes them) the
  * populated contents must match it: on any mismatch the commit is refused with
  * GMS_ERR_INTEGRITY, *mismatch_count_out (host, may be NULL) holds the count, and the
@@ -515,13 +515,17 @@ const uint64_t *gms_store_block_hashes(const gms_store *s);
  * the state before they use it.  A writer takes memory with gms_client_alloc (first fit in
  * slabs of GMS_IPC_PIECE_BYTES; a request above half a slab gets an allocation of its own;
  * GMS_ERR_SIZE above GMS_IPC_PIECE_BYTES), populates it, and commits entries (each inside
- * one of its allocations): the library hashes every 4 KiB block of them (and compares with
+ * one of its allocations): the library synchronizes the device (every write of the writer
+ * process, on any stream, has landed), hashes every 4 KiB block of them (and compares with
  * expected_blk when given, refusing the commit on a mismatch with GMS_ERR_INTEGRITY while
- * the writer keeps its lease), synchronizes the device, and the owner records the layout
- * and the hashes; the write lease ends (the writer must not write after it).  A client's
+ * the writer keeps its lease), and the owner records the layout and the hashes; the write
+ * lease ends (the writer must not write after it).  A client's
  * layout is the committed entries at its own addresses (gms_client_layout,
  * gms_client_manifest for gms_restore / gms_verify; empty before the first commit): a
- * reader's to use, a writer's to repopulate.  With GMS_CONNECT_VERIFY a reader re-hashes
+ * reader's to use, a writer's to repopulate.  A writer that took over committed state gets
+ * its slabs back with the committed entries as their allocated parts (the rest free), and
+ * freeing memory that a committed entry uses drops the client's layout and manifest (no
+ * later call can then reach the freed memory through them).  With GMS_CONNECT_VERIFY a reader re-hashes
  * the layout against the commit-time hashes before the lease is granted, and any mismatch
  * refuses the lease (GMS_ERR_INTEGRITY, the count in *mismatch_count_out) and invalidates
  * the committed state at the owner until a writer commits again.  gms_client_verify

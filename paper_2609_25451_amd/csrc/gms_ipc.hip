@@ -243,9 +243,12 @@ uint64_t round_up(uint64_t v, uint64_t a) { return (v + a - 1) / a * a; }
 
 namespace {
 
+constexpr uint64_t kAllocSlab = 1;  // allocation flag: the writer suballocates it
+
 struct OwnedAlloc {
     uint64_t bytes = 0;  // as requested; the handle holds them rounded to the granularity
     uint64_t size = 0;   // the handle's size
+    uint64_t flags = 0;  // kAllocSlab, as the writer asked; kept for later writers
     hipMemGenericAllocationHandle_t handle{};
 };
 
@@ -321,7 +324,7 @@ hipError_t export_fd(hipMemGenericAllocationHandle_t h, int *fd)
 }
 
 // A descriptor per allocation, in allocation-id order, with the table
-// {id, bytes, size} in `out`.
+// {id, bytes, size, flags} in `out`.
 int export_all(gms_owner *o, Out &out, std::vector<int> &fds)
 {
     out.put((uint64_t)o->allocs.size());
@@ -330,6 +333,7 @@ int export_all(gms_owner *o, Out &out, std::vector<int> &fds)
         out.put(kv.first);
         out.put(a.bytes);
         out.put(a.size);
+        out.put(a.flags);
         int fd = -1;
         DeviceGuard g(o->device);
         hipError_t e = export_fd(a.handle, &fd);
@@ -454,6 +458,7 @@ int handle(gms_owner *o, Conn &c, const Wire &w, const std::vector<uint8_t> &pay
         OwnedAlloc a;
         a.bytes = bytes;
         a.size = round_up(bytes, o->gran);
+        a.flags = w.arg[1] & kAllocSlab;
         hipMemAllocationProp prop = shareable_prop(o->device);
         DeviceGuard g(o->device);
         hipError_t e = hipMemCreate(&a.handle, a.size, &prop, 0);
@@ -471,6 +476,7 @@ int handle(gms_owner *o, Conn &c, const Wire &w, const std::vector<uint8_t> &pay
         out.put(id);
         out.put(a.bytes);
         out.put(a.size);
+        out.put(a.flags);
         o->allocs[id] = a;
         Wire r;
         r.op = w.op;
@@ -732,7 +738,7 @@ int map_alloc(gms_client *c, ClientAlloc &a, int fd)
     return GMS_OK;
 }
 
-// Reads an allocation table {count, then id, bytes, size each} and maps every
+// Reads an allocation table {count, then id, bytes, size, flags each} and maps every
 // allocation, taking the descriptors from `fds` in order (more arrive in kFds
 // messages when needed).
 int map_table(gms_client *c, In &in, std::vector<int> &fds, uint64_t nfds)
@@ -746,8 +752,10 @@ int map_table(gms_client *c, In &in, std::vector<int> &fds, uint64_t nfds)
     if (!in.get(n) || n > fds.size()) return fail(GMS_ERR_IO, "short reply from the owner");
     for (uint64_t i = 0; i < n; ++i) {
         ClientAlloc a;
-        if (!in.get(a.id) || !in.get(a.bytes) || !in.get(a.size) || a.bytes > a.size)
+        uint64_t flags = 0;
+        if (!in.get(a.id) || !in.get(a.bytes) || !in.get(a.size) || !in.get(flags) || a.bytes > a.size)
             return fail(GMS_ERR_IO, "short reply from the owner");
+        a.slab = (flags & kAllocSlab) != 0;
         if (c->device != GMS_HOST_ONLY) {
             int rc = map_alloc(c, a, fds[i]);
             if (rc != GMS_OK) return rc;
@@ -780,6 +788,55 @@ void teardown(gms_client *c)
     c->d_hash = c->d_count = nullptr;
     c->allocs.clear();
     c->layout.clear();
+}
+
+// Forgets the committed layout (its manifest and hashes): a writer that frees memory the
+// layout uses no longer has it whole.
+void drop_committed(gms_client *c)
+{
+    if (c->device != GMS_HOST_ONLY) {
+        DeviceGuard g(c->device);
+        (void)hipDeviceSynchronize();
+        if (c->m) gms_manifest_destroy(c->m);
+        if (c->d_hash) (void)hipFree(c->d_hash);
+    }
+    c->m = nullptr;
+    c->d_hash = nullptr;
+    c->layout.clear();
+}
+
+bool layout_touches(const gms_client *c, uint64_t lo, uint64_t hi)
+{
+    for (const gms_entry &e : c->layout)
+        if (e.nbytes && e.addr < hi && e.addr + e.nbytes > lo) return true;
+    return false;
+}
+
+// A writer that took over committed state: the parts of its slabs are the
+// committed entries in them (rounded up to the default alignment, short of the
+// next entry), the rest is free.
+void rebuild_slabs(gms_client *c)
+{
+    for (auto &kv : c->allocs) {
+        ClientAlloc &a = kv.second;
+        if (!a.slab) continue;
+        a.parts.clear();
+        a.free.clear();
+        std::map<uint64_t, uint64_t> in;  // offset -> bytes of the entries in this slab
+        for (const gms_entry &e : c->layout)
+            if (e.nbytes && e.addr >= a.va && e.addr < a.va + a.bytes) in[e.addr - a.va] = e.nbytes;
+        for (auto it = in.begin(); it != in.end(); ++it) {
+            auto nx = std::next(it);
+            const uint64_t end = nx == in.end() ? a.bytes : nx->first;  // entries do not overlap
+            a.parts[it->first] = std::min(round_up(it->second, 256), end - it->first);
+        }
+        uint64_t at = 0;
+        for (const auto &p : a.parts) {
+            if (p.first > at) a.free[at] = p.first - at;
+            at = std::max(at, p.first + p.second);
+        }
+        if (a.bytes > at) a.free[at] = a.bytes - at;
+    }
 }
 
 // Verify the mapped state against the commit-time hashes.
@@ -894,6 +951,7 @@ int gms_client_connect(const char *socket_path, int mode, uint32_t flags, void *
         delete c;
         return rc;
     }
+    if (mode == GMS_LEASE_RW) rebuild_slabs(c);
     *out = c;
     return GMS_OK;
 }
@@ -940,6 +998,7 @@ int gms_client_alloc(gms_client *c, uint64_t bytes, uint64_t align, uint64_t *ad
     Wire w, r;
     w.op = kAlloc;
     w.arg[0] = slab ? GMS_IPC_PIECE_BYTES : need;
+    w.arg[1] = slab ? kAllocSlab : 0;
     std::vector<uint8_t> rp;
     std::vector<int> fds;
     int rc = request(c, w, nullptr, r, rp, fds);
@@ -981,6 +1040,7 @@ int gms_client_free(gms_client *c, uint64_t addr)
             auto p = a.parts.find(addr - a.va);
             if (p == a.parts.end()) break;
             uint64_t off = p->first, len = p->second;
+            if (layout_touches(c, a.va + off, a.va + off + len)) drop_committed(c);
             a.parts.erase(p);
             auto nx = a.free.lower_bound(off);
             if (nx != a.free.end() && nx->first == off + len) {
@@ -999,6 +1059,7 @@ int gms_client_free(gms_client *c, uint64_t addr)
         }
         if (addr != a.va) break;
         const uint64_t id = kv.first;
+        if (layout_touches(c, a.va, a.va + a.bytes)) drop_committed(c);
         {
             DeviceGuard g(c->device);
             (void)hipDeviceSynchronize();
@@ -1054,9 +1115,15 @@ int gms_client_commit(gms_client *c, const gms_entry *entries, uint64_t n, const
         gms_manifest *m = nullptr;
         int rc = gms::manifest_create(entries, n, c->device, 0, false, &m);  // entries checked above
         if (rc != GMS_OK) return rc;
+        // every device write of this process, on any stream, lands before it is hashed
+        hipError_t e = hipDeviceSynchronize();
+        if (e != hipSuccess) {
+            gms_manifest_destroy(m);
+            return fail_hip(e, "hipDeviceSynchronize");
+        }
         const uint64_t nb = gms_num_blocks(m);
         uint64_t *d = nullptr, *cnt = nullptr;
-        hipError_t e = hipMalloc((void **)&d, std::max<uint64_t>(nb, 1) * 8);
+        e = hipMalloc((void **)&d, std::max<uint64_t>(nb, 1) * 8);
         if (e == hipSuccess) e = hipMalloc((void **)&cnt, 8);
         if (e != hipSuccess) {
             (void)hipGetLastError();
@@ -1083,8 +1150,6 @@ int gms_client_commit(gms_client *c, const gms_entry *entries, uint64_t n, const
             return fail(GMS_ERR_INTEGRITY, "%llu blocks differ from the expected hashes; commit refused",
                         (unsigned long long)count);
         }
-        // every write of this process lands before the state is published
-        if ((e = hipDeviceSynchronize()) != hipSuccess) return fail_hip(e, "hipDeviceSynchronize");
     }
     out.put((uint64_t)hs.size());
     out.put_raw(hs.data(), hs.size() * 8);

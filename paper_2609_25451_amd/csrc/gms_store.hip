@@ -225,7 +225,9 @@ int gms_store_commit(gms_store *s, uint64_t lease, const gms_entry *entries, uin
         return fail(GMS_ERR_NOMEM, "store block hashes (%llu): %s", (unsigned long long)nb, hipGetErrorString(e));
     }
     uint64_t count = 0;
-    rc = hash_and_compare(s, m, expected_blk, hash, nullptr, 0, &count, stream);
+    // every device write of the writer, on any stream, lands before it is hashed
+    if ((e = hipDeviceSynchronize()) != hipSuccess) rc = fail_hip(e, "hipDeviceSynchronize");
+    if (rc == GMS_OK) rc = hash_and_compare(s, m, expected_blk, hash, nullptr, 0, &count, stream);
     if (rc == GMS_OK && count) {
         rc = fail(GMS_ERR_INTEGRITY, "%llu blocks differ from the expected hashes; commit refused",
                   (unsigned long long)count);

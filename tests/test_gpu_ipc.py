@@ -129,6 +129,33 @@ c.commit(lay, expected=exp)
 print("recommitted", flush=True)
 """
 
+_RESHAPER = _COMMON + r"""
+# a writer that takes over committed state gets its slabs back with the committed entries as
+# their parts: it frees one entry inside a slab and the entry with an allocation of its own,
+# allocates both again, repopulates and commits a layout that moved
+c = gms.Client(SOCK, gms.LEASE_RW)
+lay = c.layout()
+assert [n for _, n in lay] == sizes() and c.manifest() is not None
+try:  # inside a slab but not the start of a part
+    c.free(lay[0][0] + 8)
+    raise SystemExit("freed a middle address")
+except gms.GmsError as e:
+    assert e.status == gms.GMS_ERR_INVALID, e.status
+c.free(lay[0][0])
+assert c.layout() == [] and c.manifest() is None  # the committed layout is no longer whole
+c.free(lay[-2][0])
+keep = lay[1:-2] + [lay[-1]]
+new0 = c.alloc(sizes()[0])
+for a, n in keep:  # the new part lies outside every entry that stays
+    assert new0 + sizes()[0] <= a or a + n <= new0, (new0, a, n)
+newbig = c.alloc(BIG)
+addrs = [new0] + [a for a, _ in lay[1:-2]] + [newbig, lay[-1][0]]
+fill(addrs)
+o_blk, _ = oracle.hashes(reference())
+c.commit(list(zip(addrs, sizes())), expected=torch.from_numpy(o_blk.view(np.int64)).cuda())
+print("reshaped", flush=True)
+"""
+
 _CORRUPTER = _COMMON + r"""
 # stands for a fault that changes committed memory behind the protocol's back: this reader
 # writes one byte of entry 3 through its own mapping (nothing in the library would)
@@ -294,4 +321,16 @@ def test_changed_state_is_refused_until_a_writer_repairs_it(owner):
     print("repairing writer", flush=True)
     assert "repaired" in _finish(_spawn(_REPAIRER, owner))
     assert gms.owner_query(owner)[:3] == ("COMMITTED", 0, False)
+    _finish(_spawn(_READER, owner))
+
+
+def test_writer_takes_over_committed_slabs_frees_and_reallocates(owner):
+    """A writer from committed state frees committed entries (one inside a slab, one with an
+    allocation of its own) and allocates again; its layout and manifest are dropped at the
+    first free, and the new layout commits and verifies in a reader."""
+    _finish(_spawn(_WRITER, owner))
+    allocs = gms.owner_query(owner)[3]
+    print("reshaping writer", flush=True)
+    assert "reshaped" in _finish(_spawn(_RESHAPER, owner))
+    assert gms.owner_query(owner)[:3] == ("COMMITTED", 0, False) and gms.owner_query(owner)[3] == allocs
     _finish(_spawn(_READER, owner))

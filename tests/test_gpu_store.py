@@ -96,6 +96,37 @@ def test_commit_readers_and_rewrite():
     s.close()
 
 
+def test_commit_waits_for_writes_still_queued_on_other_streams():
+    """Commit turns every mapping of the store read-only.  Device writes the writer queued on
+    another stream land first, also with an empty committed layout (no hashing launch to
+    order them), and then the pages hold exactly what those writes left."""
+    need_gpu()
+    s = gms.Store(va_bytes=1 << 30, slab_bytes=SLAB)
+    w = s.connect_rw()
+    n = 128 << 20
+    a = w.alloc(n)
+    side = torch.cuda.Stream()
+    for seed in range(12):  # a queue of whole-range writes, still running at commit
+        synth.dev_fill_bytes(a, n, seed, 9, stream=side)
+    w.commit([])
+    assert s.state() == ("COMMITTED", 0, False)
+    assert np.array_equal(d2h(a, n), synth.random_bytes(n, 11, 9))
+    # the same with the range in the layout: commit hashes what the last write left
+    w = s.connect_rw()
+    a = w.alloc(n)
+    want = synth.random_bytes(n, 23, 9)
+    o_blk, _ = oracle.hashes([want])
+    exp = torch.from_numpy(o_blk.view(np.int64)).cuda()
+    torch.cuda.synchronize()
+    for seed in range(12, 24):
+        synth.dev_fill_bytes(a, n, seed, 9, stream=side)
+    w.commit([(a, n)], expected=exp)
+    assert s.state() == ("COMMITTED", 0, False)
+    assert np.array_equal(_store_hashes(s, s.layout()), o_blk)
+    w.close()
+    s.close()
+
+
 def test_commit_refused_on_expected_hash_mismatch():
     """A writer that populated from an image commits against the image's hashes;
     a corrupted byte refuses the commit and the writer keeps its lease."""
