@@ -234,6 +234,62 @@ __device__ __forceinline__ void store_block(const u32x4 v[4], gbyte *p)
     for (int k = 0; k < 4; ++k) __builtin_nontemporal_store(v[k], (gvec *)(p + k * 1024));
 }
 
+// An interior block of the shifted path (see move_block_shifted): a restore's
+// full block that is not its chunk's last, or any full block of a snapshot or
+// verify.  Every granule is whole (bar a chunk's first, for a restore), so no
+// segment needs bounds.  The join takes bytes o .. o + 15 of each segment pair,
+// o = 4 * D + r, o = 16 - a for a restore and a otherwise.
+template <int OP, bool HASH, int D>
+__device__ __forceinline__ uint64_t interior_block(uint32_t b, gbyte *img, gbyte *gran, uint64_t jg0, uint64_t gblk,
+                                                   const HashOut &h, uint32_t lane, bool check, uint32_t a,
+                                                   uint32_t r)
+{
+    const u32x4 zero = {0u, 0u, 0u, 0u};
+    u32x4 seg[4];
+    if (OP == kRestore) {
+#pragma unroll
+        for (int k = 0; k < 4; ++k) seg[k] = __builtin_nontemporal_load((const gvec *)(img + k * 1024));
+        const bool inner = b > 0;  // the chunk's previous block shares granule 0
+        u32x4 before = zero;
+        if (inner && lane == 0) before = *(const gvec *)(img - 16);
+        u32x4 rot[4];
+#pragma unroll
+        for (int k = 0; k < 4; ++k) rot[k] = rotate<kWaveRor1>(seg[k]);
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+            const u32x4 prev = lane == 0 ? (k > 0 ? rot[k - 1] : before) : rot[k];
+            const u32x4 gv = join_at<D>(prev, seg[k], r);
+            if (k == 0 && !inner && lane == 0)
+                store_range(gran, gv, (int)a, 16);
+            else
+                __builtin_nontemporal_store(gv, (gvec *)(gran + k * 1024));
+        }
+    } else {
+        u32x4 g[4];
+#pragma unroll
+        for (int k = 0; k < 4; ++k) g[k] = __builtin_nontemporal_load((const gvec *)(gran + k * 1024));
+        u32x4 tail = zero;  // the granule after the block, for lane 63
+        if (lane == 63) tail = *(const gvec *)(gran + 3 * 1024 + 16);
+        u32x4 rot[4];
+#pragma unroll
+        for (int k = 0; k < 4; ++k) rot[k] = rotate<kWaveRol1>(g[k]);
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+            const u32x4 next = lane == 63 ? (k < 3 ? rot[k + 1] : tail) : rot[k];
+            seg[k] = join_at<D>(g[k], next, r);
+            if (OP == kSnapshot) __builtin_nontemporal_store(seg[k], (gvec *)(img + k * 1024));
+        }
+    }
+    uint64_t tacc = 0;
+    if (HASH) {
+        uint64_t hl = 0;
+#pragma unroll
+        for (int k = 0; k < 4; ++k) hl ^= seg_hash(seg[k], jg0 + (uint64_t)k * kSegStrideG);
+        tacc = finish_block(hl, gblk, h, lane, check, check ? h.expected[gblk] : 0);
+    }
+    return tacc;
+}
+
 // Block b of a chunk whose entry address is not 16-byte aligned (a = addr mod
 // 16, 1..15).  Image slots are 4096-aligned, so the image side stays in
 // 16-byte segments that hold whole entry words: lane l's segment s = 64k + l
@@ -270,48 +326,14 @@ __device__ __forceinline__ uint64_t move_block_shifted(const Chunk &c, uint32_t 
     // the one after it, which holds the block's last a bytes.
     const bool interior = OP == kRestore ? bs + kBlockBytes < c.len : bs + kBlockBytes <= c.len;
     if (interior) {
-        if (OP == kRestore) {
-#pragma unroll
-            for (int k = 0; k < 4; ++k) seg[k] = __builtin_nontemporal_load((const gvec *)(img + k * 1024));
-            const bool inner = b > 0;
-            u32x4 before = zero;
-            if (inner && lane == 0) before = *(const gvec *)(img - 16);
-            u32x4 r[4];
-#pragma unroll
-            for (int k = 0; k < 4; ++k) r[k] = rotate<kWaveRor1>(seg[k]);
-#pragma unroll
-            for (int k = 0; k < 4; ++k) {
-                const u32x4 prev = lane == 0 ? (k > 0 ? r[k - 1] : before) : r[k];
-                const u32x4 gv = join(prev, seg[k], 16 - a);
-                if (k == 0 && !inner && lane == 0)
-                    store_range(gran, gv, (int)a, 16);
-                else
-                    __builtin_nontemporal_store(gv, (gvec *)(gran + k * 1024));
-            }
-        } else {
-            u32x4 g[4];
-#pragma unroll
-            for (int k = 0; k < 4; ++k) g[k] = __builtin_nontemporal_load((const gvec *)(gran + k * 1024));
-            u32x4 tail = zero;
-            if (lane == 63) tail = *(const gvec *)(gran + 3 * 1024 + 16);
-            u32x4 n[4];
-#pragma unroll
-            for (int k = 0; k < 4; ++k) n[k] = rotate<kWaveRol1>(g[k]);
-#pragma unroll
-            for (int k = 0; k < 4; ++k) {
-                const u32x4 next = lane == 63 ? (k < 3 ? n[k + 1] : tail) : n[k];
-                seg[k] = join(g[k], next, a);
-                if (OP == kSnapshot) __builtin_nontemporal_store(seg[k], (gvec *)(img + k * 1024));
-            }
+        // one straight-line body per dword shift of the join (the shift is fixed per chunk)
+        const uint32_t o = OP == kRestore ? 16 - a : a;
+        switch (o >> 2) {
+        case 0: return interior_block<OP, HASH, 0>(b, img, gran, jg0, gblk, h, lane, check, a, o & 3);
+        case 1: return interior_block<OP, HASH, 1>(b, img, gran, jg0, gblk, h, lane, check, a, o & 3);
+        case 2: return interior_block<OP, HASH, 2>(b, img, gran, jg0, gblk, h, lane, check, a, o & 3);
+        default: return interior_block<OP, HASH, 3>(b, img, gran, jg0, gblk, h, lane, check, a, o & 3);
         }
-        uint64_t tacc = 0;
-        if (HASH) {
-            uint64_t hl = 0;
-#pragma unroll
-            for (int k = 0; k < 4; ++k) hl ^= seg_hash(seg[k], jg0 + (uint64_t)k * kSegStrideG);
-            tacc = finish_block(hl, gblk, h, lane, check, check ? h.expected[gblk] : 0);
-        }
-        return tacc;
     }
 
     if (OP == kRestore) {
