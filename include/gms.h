@@ -151,6 +151,19 @@ uint64_t gms_num_chunks(const gms_manifest *m);    /* work items                
  * launched apart once the idle units they would otherwise leave outweigh a
  * launch; a manifest of similar chunks is one launch. */
 uint64_t gms_num_launch_groups(const gms_manifest *m);
+/* Launch group g (0 <= g < gms_num_launch_groups): its chunks, its work units per
+ * chunk as a power of two (0: one unit per chunk, a paired launch), and flags:
+ * GMS_GROUP_SHIFTED (entries off a 16-byte boundary, the byte-shifting kernels) and
+ * GMS_GROUP_STRIPED (restores take the striped unit order: the group's chunks span
+ * several work units and are mostly entries of their own, such as a KV pool's live
+ * units).  Outputs may be NULL.
+ * Errors: GMS_ERR_INVALID (manifest null, g out of range). */
+enum gms_group_flags {
+    GMS_GROUP_SHIFTED = 1,
+    GMS_GROUP_STRIPED = 2
+};
+int gms_launch_group(const gms_manifest *m, uint64_t g, uint64_t *chunks_out, uint32_t *unit_shift_out,
+                     uint32_t *flags_out);
 int gms_manifest_device(const gms_manifest *m);
 
 /* Copies img_off[n] and blk_base[n] (host arrays; either may be NULL). */
@@ -585,7 +598,7 @@ const char *gms_last_error(void);
 
 /* ABI version of this header (2: adds the model-state store and GMS_ERR_INTEGRITY;
  * 3: adds gms_restore_from_host and gms_snapshot_to_host; 4: adds gms_restore_pinned_noalloc,
- * the owner process and its clients). */
+ * the owner process and its clients; 5: adds gms_launch_group). */
 int gms_abi_version(void);
 
 #ifdef __cplusplus

@@ -50,6 +50,8 @@ FILE_DIRECT = 1
 FILE_SYNC = 2
 MEM_DEVICE = 0
 MEM_HOST_PINNED = 1
+GROUP_SHIFTED = 1  # gms_group_flags
+GROUP_STRIPED = 2
 HOST_ONLY = -1
 BLOCK_BYTES = 4096
 DEFAULT_SLICE_BYTES = 256 << 20  # GMS_DEFAULT_SLICE_BYTES
@@ -75,6 +77,7 @@ _image_bytes = _sig("gms_image_bytes", U64, [VP])
 _num_blocks = _sig("gms_num_blocks", U64, [VP])
 _num_chunks = _sig("gms_num_chunks", U64, [VP])
 _num_groups = _sig("gms_num_launch_groups", U64, [VP])
+_launch_group = _sig("gms_launch_group", INT, [VP, U64, VP, VP, VP])
 _device = _sig("gms_manifest_device", INT, [VP])
 _layout = _sig("gms_layout", INT, [VP, VP, VP])
 _set_staging = _sig("gms_manifest_set_staging", INT, [VP, U64, ctypes.c_uint32])
@@ -323,6 +326,16 @@ class Manifest:
     @property
     def num_launch_groups(self) -> int:
         return int(_num_groups(self._h))
+
+    def launch_groups(self) -> list:
+        """Per launch group: {"chunks", "unit_shift", "shifted", "striped"}."""
+        out = []
+        for g in range(self.num_launch_groups):
+            n, sh, fl = U64(), ctypes.c_uint32(), ctypes.c_uint32()
+            _check(_launch_group(self._h, g, ctypes.byref(n), ctypes.byref(sh), ctypes.byref(fl)), "gms_launch_group")
+            out.append({"chunks": int(n.value), "unit_shift": int(sh.value), "shifted": bool(fl.value & GROUP_SHIFTED),
+                        "striped": bool(fl.value & GROUP_STRIPED)})
+        return out
 
     @property
     def device(self) -> int:

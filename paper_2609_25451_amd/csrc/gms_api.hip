@@ -174,25 +174,37 @@ void plan_launch_groups(gms_manifest *m)
     if (plan.size() == 1) {
         plan[0].count = n;
         m->groups.push_back(plan[0]);
-        return;
+    } else {
+        // chunks by group, in image order within a group
+        std::vector<Chunk> sorted;
+        sorted.reserve(n);
+        for (LaunchGroup lg : plan) {
+            lg.first = sorted.size();
+            for (uint64_t i = 0; i < n; ++i)
+                if (group_of[cls[i]] == lg.shift && shifted(i) == lg.shifted) sorted.push_back(m->chunks[i]);
+            lg.count = sorted.size() - lg.first;
+            m->groups.push_back(lg);
+        }
+        m->chunks.swap(sorted);
     }
-    // chunks by group, in image order within a group
-    std::vector<Chunk> sorted;
-    sorted.reserve(n);
-    for (LaunchGroup lg : plan) {
-        lg.first = sorted.size();
-        for (uint64_t i = 0; i < n; ++i)
-            if (group_of[cls[i]] == lg.shift && shifted(i) == lg.shifted) sorted.push_back(m->chunks[i]);
-        lg.count = sorted.size() - lg.first;
-        m->groups.push_back(lg);
+    // A group whose chunks are mostly whole entries of their own (a KV pool's
+    // live units: destinations scattered over the pool) restores in the
+    // striped unit order; one of large tensors cut into many chunks keeps the
+    // contiguous eighths.  The chunks of an entry are adjacent in a group.
+    // Paired launches (one unit per chunk) keep their own order.
+    for (LaunchGroup &lg : m->groups) {
+        uint64_t entries = 0;
+        for (uint64_t i = lg.first; i < lg.first + lg.count; ++i)
+            entries += i == lg.first || m->chunks[i].entry != m->chunks[i - 1].entry;
+        lg.striped = lg.shift > 0 && lg.count && 2 * entries >= lg.count;
     }
-    m->chunks.swap(sorted);
 }
 
 hipError_t launch_all(const gms_manifest *m, int op, const HashOut &h, uint8_t *img_base, hipStream_t s)
 {
     for (const LaunchGroup &g : m->groups) {
-        hipError_t e = launch_stream(op, h.any(), g.shifted, m->d_chunks, g.first, g.count, g.shift, img_base, 0, h, s);
+        hipError_t e =
+            launch_stream(op, h.any(), g.shifted, g.striped, m->d_chunks, g.first, g.count, g.shift, img_base, 0, h, s);
         if (e != hipSuccess) return e;
     }
     return hipSuccess;
@@ -204,8 +216,8 @@ hipError_t launch_slice(const gms_manifest *m, int op, const HashOut &h, uint64_
     for (size_t g = 0; g < m->groups.size(); ++g) {
         const uint64_t c0 = m->slice_first[g * stride + sl], c1 = m->slice_first[g * stride + sl + 1];
         hipError_t e =
-            launch_stream(op, h.any(), m->groups[g].shifted, m->d_chunks, c0, c1 - c0, m->groups[g].shift, slot,
-                          sl * m->ring_slice, h, s);
+            launch_stream(op, h.any(), m->groups[g].shifted, m->groups[g].striped, m->d_chunks, c0, c1 - c0,
+                          m->groups[g].shift, slot, sl * m->ring_slice, h, s);
         if (e != hipSuccess) return e;
     }
     return hipSuccess;
@@ -459,7 +471,7 @@ using gms::make_hash;
 
 extern "C" {
 
-int gms_abi_version(void) { return 4; }
+int gms_abi_version(void) { return 5; }
 
 const char *gms_status_str(int status)
 {
@@ -626,6 +638,20 @@ uint64_t gms_image_bytes(const gms_manifest *m) { return m ? m->image_bytes : 0;
 uint64_t gms_num_blocks(const gms_manifest *m) { return m ? m->num_blocks : 0; }
 uint64_t gms_num_chunks(const gms_manifest *m) { return m ? (uint64_t)m->chunks.size() : 0; }
 uint64_t gms_num_launch_groups(const gms_manifest *m) { return m ? (uint64_t)m->groups.size() : 0; }
+
+int gms_launch_group(const gms_manifest *m, uint64_t g, uint64_t *chunks_out, uint32_t *unit_shift_out,
+                     uint32_t *flags_out)
+{
+    gms::clear_error();
+    if (!m || g >= m->groups.size())
+        return fail(GMS_ERR_INVALID, "launch group %llu of %llu", (unsigned long long)g,
+                    (unsigned long long)(m ? m->groups.size() : 0));
+    const gms::LaunchGroup &lg = m->groups[g];
+    if (chunks_out) *chunks_out = lg.count;
+    if (unit_shift_out) *unit_shift_out = lg.shift;
+    if (flags_out) *flags_out = (lg.shifted ? GMS_GROUP_SHIFTED : 0u) | (lg.striped ? GMS_GROUP_STRIPED : 0u);
+    return GMS_OK;
+}
 int gms_manifest_device(const gms_manifest *m) { return m ? m->device : GMS_HOST_ONLY; }
 
 int gms_layout(const gms_manifest *m, uint64_t *img_off, uint64_t *blk_base)

@@ -48,8 +48,8 @@ hipError_t launch_prologue(const HashOut &h, uint64_t n_entries, hipStream_t s);
 // selects the hashing variant; `shifted` is set when the chunks' entry
 // addresses are not 16-byte aligned and clear when they all are (a launch
 // never mixes the two).
-hipError_t launch_stream(int op, bool hash, bool shifted, const Chunk *chunks, uint64_t first, uint64_t count,
-                         uint32_t unit_shift, uint8_t *img_base, uint64_t img_origin, const HashOut &h,
+hipError_t launch_stream(int op, bool hash, bool shifted, bool striped, const Chunk *chunks, uint64_t first,
+                         uint64_t count, uint32_t unit_shift, uint8_t *img_base, uint64_t img_origin, const HashOut &h,
                          hipStream_t s);
 
 }  // namespace gms

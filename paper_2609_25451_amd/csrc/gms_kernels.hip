@@ -492,9 +492,11 @@ __device__ __forceinline__ uint64_t xcd_slot()
 // the entries together.  The last, partial round of stripes is split into eight
 // contiguous pieces, which keeps the order a permutation of the round's slots.
 // Measured on the llama8b set over six image allocations: 90.4 to 91.8% of HBM
-// peak against 86.8 to 88.8% with contiguous eighths.  Restore and snapshot keep
-// the eighths: striping them narrowed their spread at the same mean on llama8b and
-// lost up to 2.9 points on the 70B shard.
+// peak against 86.8 to 88.8% with contiguous eighths.  Restores of launch groups
+// whose chunks are mostly entries of their own (`striped`, set by the manifest:
+// a KV pool's live units) take it too, 1.2 to 1.6 points above the eighths on
+// the KV pool; weight sets keep the eighths, where striping moved llama8b by
+// -1.0 to +0.0 points and the 70B shard by -2.9 to +1.5.  Snapshots keep them.
 constexpr uint64_t kVerifyStripe = 128;
 
 __device__ __forceinline__ uint64_t striped_slot()
@@ -508,11 +510,12 @@ __device__ __forceinline__ uint64_t striped_slot()
 // Unit u is blocks [(u mod 2^shift) * kWaves, +kWaves) of chunk u >> shift
 // (2^shift units cover the launch's longest chunk); wave w of the workgroup
 // takes the unit's block w.  Tensor hashes combine the two waves' block
-// hashes in LDS and take one atomic XOR per unit.
+// hashes in LDS and take one atomic XOR per unit.  `striped` (uniform) selects
+// the striped unit order for a restore.
 template <int OP, bool HASH, bool SHIFTED>
 __global__ void __launch_bounds__(kUnitThreads)
 k_stream(const Chunk *__restrict__ chunks, uint64_t count, uint32_t unit_shift, gbyte *__restrict__ img_base,
-         uint64_t img_origin, HashOut h)
+         uint64_t img_origin, HashOut h, uint32_t striped)
 {
     extern __shared__ uint64_t wave_part[];  // kWaves words used
     const uint32_t lane = threadIdx.x & 63;
@@ -521,7 +524,7 @@ k_stream(const Chunk *__restrict__ chunks, uint64_t count, uint32_t unit_shift, 
     const uint64_t *const exp_dummy = (const uint64_t *)chunks;  // any readable word
     const uint64_t units = count << unit_shift;
     const uint32_t unit_mask = (1u << unit_shift) - 1;
-    const uint64_t slot_in_round = OP == kVerify ? striped_slot() : xcd_slot();
+    const uint64_t slot_in_round = OP == kVerify || (OP == kRestore && striped) ? striped_slot() : xcd_slot();
     for (uint64_t round = 0; round < units; round += gridDim.x) {
         const uint64_t u = round + slot_in_round;
         if (u >= units) break;  // uniform across the workgroup
@@ -647,7 +650,7 @@ uint64_t grid_for(uint64_t units)
 
 template <int OP, bool HASH, bool SHIFTED>
 hipError_t launch_t(const Chunk *chunks, uint64_t first, uint64_t count, uint32_t unit_shift, uint8_t *img_base,
-                    uint64_t img_origin, const HashOut &h, hipStream_t s)
+                    uint64_t img_origin, const HashOut &h, bool striped, hipStream_t s)
 {
     if (unit_shift == 0) {
         const uint64_t grid = grid_for((count + kWaves - 1) / kWaves);
@@ -658,7 +661,7 @@ hipError_t launch_t(const Chunk *chunks, uint64_t first, uint64_t count, uint32_
     constexpr size_t lds = OP == kVerify ? kLdsVerify : kLdsCopy;
     static_assert(lds <= 64 * 1024, "above 64 KiB the launch would have to opt in per device");
     hipLaunchKernelGGL((k_stream<OP, HASH, SHIFTED>), dim3((uint32_t)grid_for(count << unit_shift)), dim3(kUnitThreads), lds,
-                       s, chunks + first, count, unit_shift, (gbyte *)img_base, img_origin, h);
+                       s, chunks + first, count, unit_shift, (gbyte *)img_base, img_origin, h, striped ? 1u : 0u);
     return hipGetLastError();
 }
 
@@ -689,25 +692,28 @@ hipError_t launch_prologue(const HashOut &h, uint64_t n_entries, hipStream_t s)
 
 template <bool SHIFTED>
 hipError_t launch_op(int op, bool hash, const Chunk *chunks, uint64_t first, uint64_t count, uint32_t shift,
-                     uint8_t *img_base, uint64_t img_origin, const HashOut &h, hipStream_t s)
+                     uint8_t *img_base, uint64_t img_origin, const HashOut &h, bool striped, hipStream_t s)
 {
+#define GMS_LAUNCH(OP, HASH) launch_t<OP, HASH, SHIFTED>(chunks, first, count, shift, img_base, img_origin, h, striped, s)
     switch (op * 2 + (hash ? 1 : 0)) {
-    case kRestore * 2: return launch_t<kRestore, false, SHIFTED>(chunks, first, count, shift, img_base, img_origin, h, s);
-    case kRestore * 2 + 1: return launch_t<kRestore, true, SHIFTED>(chunks, first, count, shift, img_base, img_origin, h, s);
-    case kSnapshot * 2: return launch_t<kSnapshot, false, SHIFTED>(chunks, first, count, shift, img_base, img_origin, h, s);
-    case kSnapshot * 2 + 1: return launch_t<kSnapshot, true, SHIFTED>(chunks, first, count, shift, img_base, img_origin, h, s);
-    case kVerify * 2 + 1: return launch_t<kVerify, true, SHIFTED>(chunks, first, count, shift, img_base, img_origin, h, s);
+    case kRestore * 2: return GMS_LAUNCH(kRestore, false);
+    case kRestore * 2 + 1: return GMS_LAUNCH(kRestore, true);
+    case kSnapshot * 2: return GMS_LAUNCH(kSnapshot, false);
+    case kSnapshot * 2 + 1: return GMS_LAUNCH(kSnapshot, true);
+    case kVerify * 2 + 1: return GMS_LAUNCH(kVerify, true);
     default: return hipErrorInvalidValue;
     }
+#undef GMS_LAUNCH
 }
 
-hipError_t launch_stream(int op, bool hash, bool shifted, const Chunk *chunks, uint64_t first, uint64_t count,
-                         uint32_t shift, uint8_t *img_base, uint64_t img_origin, const HashOut &h, hipStream_t s)
+hipError_t launch_stream(int op, bool hash, bool shifted, bool striped, const Chunk *chunks, uint64_t first,
+                         uint64_t count, uint32_t shift, uint8_t *img_base, uint64_t img_origin, const HashOut &h,
+                         hipStream_t s)
 {
     if (count == 0) return hipSuccess;
     if (shift > kMaxUnitShift || (count << shift) >> shift != count) return hipErrorInvalidValue;
-    return shifted ? launch_op<true>(op, hash, chunks, first, count, shift, img_base, img_origin, h, s)
-                   : launch_op<false>(op, hash, chunks, first, count, shift, img_base, img_origin, h, s);
+    return shifted ? launch_op<true>(op, hash, chunks, first, count, shift, img_base, img_origin, h, striped, s)
+                   : launch_op<false>(op, hash, chunks, first, count, shift, img_base, img_origin, h, striped, s);
 }
 
 }  // namespace gms

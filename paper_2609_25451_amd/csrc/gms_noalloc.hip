@@ -96,8 +96,8 @@ extern "C" int gms_restore_pinned_noalloc(const gms_manifest *m, const void *ima
             return gms::fail_hip(e, "staging copy launch");
         for (const gms::LaunchGroup &lg : m->groups) {
             const uint64_t c0 = first_at(m, lg, lo), c1 = first_at(m, lg, lo + slice);
-            if ((e = gms::launch_stream(gms::kRestore, h.any(), lg.shifted, m->d_chunks, c0, c1 - c0, lg.shift,
-                                        stage, lo, h, s)) != hipSuccess)
+            if ((e = gms::launch_stream(gms::kRestore, h.any(), lg.shifted, lg.striped, m->d_chunks, c0, c1 - c0,
+                                        lg.shift, stage, lo, h, s)) != hipSuccess)
                 return gms::fail_hip(e, "kernel launch");
         }
     }

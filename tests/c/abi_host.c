@@ -21,7 +21,7 @@ int main(void)
 {
     gms_entry e[4] = {{1u << 20, 5000}, {2u << 20, 0}, {3u << 20, 8192}, {4u << 20, 1}};
     gms_manifest *m = NULL;
-    CHECK(gms_abi_version() == 4);
+    CHECK(gms_abi_version() == 5);
     CHECK(gms_manifest_create(e, 4, GMS_HOST_ONLY, 0, &m) == GMS_OK && m != NULL);
     CHECK(gms_num_entries(m) == 4);
     CHECK(gms_payload_bytes(m) == 5000 + 8192 + 1);

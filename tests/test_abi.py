@@ -22,7 +22,7 @@ def test_exports_every_declared_symbol():
     exported = {line.split()[-1] for line in out.splitlines() if line.strip()}
     missing = [s for s in declared if s not in exported]
     assert not missing, f"declared but not exported: {missing}"
-    assert gms.abi_version() == 4
+    assert gms.abi_version() == 5
 
 
 def _host_manifest(sizes, base=1 << 40, gap=0, chunk_bytes=0, align=1):
@@ -194,6 +194,30 @@ def test_launch_groups_split_only_when_idle_units_pay_for_a_launch():
     m, m1 = _host_manifest(sizes), _host_manifest(sizes[:4])
     off, _ = m.layout()
     assert off[:4] == m1.layout()[0] and m.image_bytes == m1.image_bytes + 3000 * 4096
+
+
+def test_restores_of_scattered_units_take_the_striped_order():
+    """A launch group whose chunks are mostly entries of their own (the KV pool's 64 KiB live
+    units) restores in the striped unit order; weight sets, whose tensors span many chunks,
+    keep the contiguous eighths.  The query reports every group of a manifest."""
+    p = synth.kv_pool()
+    live = synth.live_map(p.blocks, p.n_live, p.map_seed, p.map_stream)
+    ents = [((1 << 40) + l * p.layer_bytes + int(b) * p.unit_bytes, p.unit_bytes) for l in range(4) for b in live]
+    kv = gms.Manifest(ents, device=gms.HOST_ONLY)
+    assert kv.launch_groups() == [{"chunks": len(ents), "unit_shift": 3, "shifted": False, "striped": True}]
+    kv.close()
+    for name in ("llama8b", "llama70b_tp8", "moe"):
+        _, ts = synth.weight_set(name)
+        gs = _host_manifest([t.nbytes for t in ts], align=256).launch_groups()
+        assert not gs[0]["striped"] and sum(g["chunks"] for g in gs) > 0, name
+    # mixed: the large tensors' groups keep the eighths, the tiny buffers' groups are paired
+    # launches, which have an order of their own
+    gs = _host_manifest([64 << 20] * 4 + [100] * 3000, gap=2).launch_groups()
+    assert [(g["unit_shift"] > 0, g["shifted"], g["striped"]) for g in gs] == [
+        (True, False, False), (True, True, False), (False, False, False), (False, True, False)]
+    m = _host_manifest([4096])
+    assert gms._launch_group(m._h, 1, None, None, None) == gms.GMS_ERR_INVALID
+    assert gms._launch_group(None, 0, None, None, None) == gms.GMS_ERR_INVALID
 
 
 def test_binding_refuses_short_or_mistyped_outputs():
