@@ -211,10 +211,10 @@ sys.path.insert(0, sys.argv[1])
 import paper_2609_25451_amd as gms
 rng = random.Random(int(sys.argv[3]))
 held = 0
-for _ in range(25):
+for _ in range(12):
     c = gms.Client(sys.argv[2], gms.LEASE_RO)
     held += 1
-    time.sleep(rng.random() * 0.01)
+    time.sleep(rng.random() * 0.02)
     if rng.random() < 0.2:
         c._h = None  # leave without a goodbye: the connection closes when the process ends
         break
@@ -224,21 +224,21 @@ print("done", held, flush=True)
 
 
 def test_concurrent_reader_processes_keep_the_count(owner):
-    """Eight reader processes connect and leave at random, some without saying goodbye, while
+    """Six reader processes connect and leave at random, some without saying goodbye, while
     this process watches: the state is RO exactly while the count is positive, the count never
     exceeds the processes, and once they are gone the state is COMMITTED with no reader."""
     w = gms.Client(owner, gms.LEASE_RW)
     w.commit([])
     w.close()
     ps = [subprocess.Popen([sys.executable, "-c", _CHURN, ROOT, owner, str(seed)], stdout=subprocess.PIPE,
-                           stderr=subprocess.PIPE, text=True) for seed in range(8)]
+                           stderr=subprocess.PIPE, text=True) for seed in range(6)]
     seen = set()
     while any(p.poll() is None for p in ps):
         st, rd, inv = state(owner)
-        assert st in ("COMMITTED", "RO") and not inv and rd <= 8
+        assert st in ("COMMITTED", "RO") and not inv and rd <= 6
         assert (st == "RO") == (rd > 0)
         seen.add(rd)
-        time.sleep(0.002)
+        time.sleep(0.01)
     for p in ps:
         out, err = p.communicate()
         assert p.returncode == 0 and out.startswith("done"), out + err
