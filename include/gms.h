@@ -54,7 +54,10 @@
  *  - Device pointers must be hipMalloc'd memory of the manifest's device
  *    (sub-ranges of a caching allocator's blocks are fine); the library checks
  *    every range against its allocation and returns GMS_ERR_INVALID if it
- *    falls outside one.  The image base must be 16-byte aligned.
+ *    falls outside one.  The image base must be 16-byte aligned; entries may
+ *    start at any byte address (entries off a 16-byte boundary are moved by
+ *    byte-shifting kernels with the same 16-byte accesses, and no byte outside
+ *    an entry is written).
  *  - Hash/mismatch arrays are uint64_t device arrays: blk_hash has
  *    gms_num_blocks() entries, ten_hash gms_num_entries(), mismatch_count one,
  *    mismatch_list min(mismatch_cap, gms_num_blocks()) (a call records each
