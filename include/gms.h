@@ -241,7 +241,10 @@ int gms_verify(const gms_manifest *m, const uint64_t *expected_blk, uint64_t *bl
  * area) is copied into the area by a kernel reading the pinned image over the host link,
  * then scattered, hashed and compared by the kernels of gms_restore.  Arguments, outputs
  * and results are those of gms_restore with image_kind GMS_MEM_HOST_PINNED; no hipMalloc,
- * hipFree, stream or event is created, and only kernels are enqueued on `stream`.  The
+ * hipFree, stream or event is created, and only kernels are enqueued on `stream`, so the
+ * call can be captured into a HIP graph (each replay reads the pinned image anew) after
+ * one call outside capture on the device; on a manifest that an earlier staging-ring call
+ * used, a capturing call returns GMS_ERR_STATE (the graph could not wait for it).  The
  * area is shared by every call on a device: calls that overlap on one device (different
  * streams or threads) race, so a caller serializes them, for example on one stream.
  * Errors: as gms_restore, plus GMS_ERR_SIZE for staging_bytes above

@@ -81,9 +81,15 @@ extern "C" int gms_restore_pinned_noalloc(const gms_manifest *m, const void *ima
     hipError_t e;
     gms_manifest *mm = const_cast<gms_manifest *>(m);
     std::lock_guard<std::mutex> lock(mm->ring_mu);
-    // after any earlier staging-ring call on this manifest
-    if (m->done_recorded && (e = hipStreamWaitEvent(s, m->ev_done, 0)) != hipSuccess)
-        return gms::fail_hip(e, "ring order");
+    // after any earlier staging-ring call on this manifest; a graph cannot wait on
+    // that call's event, so a capturing stream is refused once there was one
+    if (m->done_recorded) {
+        hipStreamCaptureStatus cap = hipStreamCaptureStatusNone;
+        if ((e = hipStreamIsCapturing(s, &cap)) != hipSuccess) return gms::fail_hip(e, "hipStreamIsCapturing");
+        if (cap != hipStreamCaptureStatusNone)
+            return gms::fail(GMS_ERR_STATE, "capturing after a staging-ring call on this manifest");
+        if ((e = hipStreamWaitEvent(s, m->ev_done, 0)) != hipSuccess) return gms::fail_hip(e, "ring order");
+    }
     if ((e = gms::launch_prologue(h, m->n, s)) != hipSuccess) return gms::fail_hip(e, "prologue launch");
     if (m->chunks.empty()) return GMS_OK;
     uint8_t *host_dev = nullptr;  // the pinned image as the copy kernel sees it

@@ -99,3 +99,70 @@ def test_noalloc_refuses_staging_beyond_the_area():
             gms.restore_pinned_noalloc(m, pinned, staging_bytes=staging)
         assert e.value.status == gms.GMS_ERR_SIZE
     m.close()
+
+
+def test_noalloc_restore_replays_from_a_graph():
+    """After one call outside capture, the allocation-free restore captured into a HIP graph
+    replays: each replay reads the pinned image as it is at that moment, restores it and
+    compares it with the expected hashes.  Replays are checked against the oracle, with eager
+    work and a host-side change of the image between them.  On a manifest that a staging-ring
+    call used, a capturing call is refused before it records anything."""
+    need_gpu()
+    sizes = [70_000, 4096 * 5 + 3, 1, 300_001, 64 << 10, 2_000_003]
+    arena = Arena(sizes, misalign=lambda r: r.integers(0, 16) if r.random() < 0.5 else 0, gap=32, seed=77)
+    datas = random_datas(sizes, seed=77)
+    arena.fill(datas)
+    m = gms.Manifest(arena.entries, device=0)
+    pinned = torch.empty(m.image_bytes, dtype=torch.uint8, pin_memory=True)
+    pinned.numpy()[:] = oracle.pack(datas)  # written on the host: no staging-ring call on m
+    o_blk, o_ten = oracle.hashes(datas)
+    exp = from_u64(o_blk)
+    blk, ten, cnt, lst = _outputs(arena, m.num_blocks, m.num_entries)
+    side = torch.cuda.Stream()
+
+    def call():
+        gms.restore_pinned_noalloc(m, pinned, staging_bytes=1 << 20, expected=exp, blk_hash=blk, ten_hash=ten,
+                                   mismatch_count=cnt, mismatch_list=lst, mismatch_cap=16)
+
+    with torch.cuda.stream(side):
+        call()  # the eager call: also loads the kernels and finds the staging area
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g, stream=side):
+        call()
+    torch.cuda.synchronize()
+
+    off, base = m.layout()
+    scratch = torch.ones(1 << 22, device="cuda")
+    for step, flip in enumerate([False, True, False, True]):
+        want = [d.copy() for d in datas]
+        if flip:  # one byte of entry 3 changed in the image on the host
+            pinned[off[3] + 5 + step] ^= 0x10
+            want[3][5 + step] ^= 0x10
+        arena.poison()
+        scratch.mul_(1.5)  # eager work between replays
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        back, whole = arena.read()
+        assert all(np.array_equal(x, y) for x, y in zip(back, want)), step
+        assert arena.outside_untouched(whole), step
+        w_blk, w_ten = oracle.hashes(want)
+        assert np.array_equal(to_u64(blk, m.num_blocks), w_blk), step
+        assert np.array_equal(to_u64(ten, m.num_entries), w_ten), step
+        assert int(cnt.item()) == (1 if flip else 0), step
+        if flip:
+            assert to_u64(lst)[0] == base[3] + (5 + step) // 4096
+            pinned[off[3] + 5 + step] ^= 0x10  # put back
+
+    # a staging-ring call on the manifest: a graph could not wait for it, so capture is refused
+    gms.restore(m, pinned, m.image_bytes, gms.MEM_HOST_PINNED, expected=exp, mismatch_count=cnt)
+    torch.cuda.synchronize()
+    g2 = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g2, stream=side):
+        with pytest.raises(gms.GmsError) as e:
+            call()
+        scratch.add_(1.0)  # the capture still holds a node of its own
+    assert e.value.status == gms.GMS_ERR_STATE
+    torch.cuda.synchronize()
+    m.close()
