@@ -519,7 +519,10 @@ import paper_2609_25451_amd as gms
 from gpu_util import Arena, random_datas
 import test_gpu_parity as t
 rng = np.random.default_rng(77)
-sizes = [int(v) for v in rng.integers(1, 200_000, 60)] + [3 << 20, 1 << 20] + [int(v) for v in rng.integers(1, 5000, 3000)]
+# first, 3,100 entries of 16 KiB: one two-unit chunk each, a launch group of their own that restores
+# in the striped order
+sizes = [16384] * 3100
+sizes += [int(v) for v in rng.integers(1, 200_000, 60)] + [3 << 20, 1 << 20] + [int(v) for v in rng.integers(1, 5000, 3000)]
 arena = Arena(sizes, misalign=lambda r: r.integers(0, 16) if r.random() < 0.3 else 0, gap=16, seed=77)
 datas = random_datas(sizes, seed=77)
 host = np.full(arena.total, 0xA5, dtype=np.uint8)
@@ -527,6 +530,8 @@ for o, d in zip(arena.offsets, datas):
     host[o:o + d.size] = d
 arena.buf.copy_(torch.from_numpy(host))
 m, _ = t._round_trip(arena, datas, gms.MEM_DEVICE)
+gs = m.launch_groups()
+assert any(g["striped"] for g in gs) and any(g["unit_shift"] and not g["striped"] for g in gs), gs
 print("rounds ok", m.num_blocks, m.num_launch_groups, flush=True)
 """
 
