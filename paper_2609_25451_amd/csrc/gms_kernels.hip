@@ -10,7 +10,8 @@
 // dispatcher keep every CU's few resident waves busy; restore and snapshot
 // launches reserve LDS so that six workgroups (12 waves) are resident per CU,
 // which measured best for the mixed read/write stream across weight sets,
-// shards and KV pools, and the unit order is XCD-aware (striped for verify).  Hashing happens on
+// shards and KV pools, and the unit order is XCD-aware (striped for verify and for
+// restores of scattered units, contiguous per XCD otherwise).  Hashing happens on
 // the registers that were just moved: each lane mixes its eight 8-byte words,
 // the wave XOR-reduces its 64 partials with DPP row operations plus four lane
 // reads, and lane 0 stores / compares the block hash.  Tensor hashes combine
