@@ -63,6 +63,7 @@ namespace {
 constexpr uint32_t kMagic = 0x31534D47u;  // "GMS1"
 constexpr uint32_t kMaxFdsPerMsg = 128;
 constexpr uint64_t kMaxPayload = 1ull << 32;  // refuse absurd lengths from a broken peer
+constexpr uint64_t kRecvPiece = 1ull << 20;   // payload bytes received per step
 
 enum Op : uint32_t {
     kHelloRW = 1,
@@ -168,8 +169,15 @@ int recv_msg(int fd, Wire &w, std::vector<uint8_t> &payload, std::vector<int> &f
         }
     if ((size_t)k < sizeof w && recv_all(fd, (uint8_t *)&w + k, sizeof w - (size_t)k)) return -1;
     if (w.magic != kMagic || w.payload > kMaxPayload) return -1;
-    payload.resize(w.payload);
-    return w.payload ? recv_all(fd, payload.data(), w.payload) : 0;
+    // the buffer grows with the bytes that arrive, so a length alone reserves nothing
+    payload.clear();
+    for (uint64_t got = 0; got < w.payload;) {
+        const uint64_t part = std::min<uint64_t>(w.payload - got, kRecvPiece);
+        payload.resize(got + part);
+        if (recv_all(fd, payload.data() + got, part)) return -1;
+        got += part;
+    }
+    return 0;
 }
 
 void close_all(std::vector<int> &fds)
@@ -202,7 +210,7 @@ struct In {
     bool get_raw(void *d, size_t n)
     {
         if ((size_t)(end - p) < n) return false;
-        memcpy(d, p, n);
+        if (n) memcpy(d, p, n);  // an empty table's buffer may be null
         p += n;
         return true;
     }

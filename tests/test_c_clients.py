@@ -78,7 +78,8 @@ int main(void) {
 
 
 def test_host_code_under_sanitizers(tmp_path):
-    """The library's host code (validation, overlap sort, layout, chunking) under ASan/UBSan."""
+    """The library's host code under ASan/UBSan: validation, overlap sort, layout and chunking
+    (a fuzzed manifest builder), and the owner process's message handling (a fuzzed peer)."""
     lib = tmp_path / "libgms_san.so"
     srcs = sorted(os.path.join(ROOT, "paper_2609_25451_amd", "csrc", f)
                   for f in os.listdir(os.path.join(ROOT, "paper_2609_25451_amd", "csrc")) if f.endswith(".hip"))
@@ -100,3 +101,11 @@ def test_host_code_under_sanitizers(tmp_path):
     env = dict(os.environ, ASAN_OPTIONS="detect_leaks=0", UBSAN_OPTIONS="halt_on_error=1")
     r = _run([str(exe)], env=env)
     assert r.returncode == 0 and "manifest fuzz ok" in r.stdout, (r.stdout + r.stderr)[-3000:]
+    # the owner process's message handling against hostile peers, in the same sanitized build
+    exe = tmp_path / "owner_fuzz"
+    r = _run([clang, "-std=c99", "-O1", "-g", "-pthread", "-fsanitize=address,undefined", "-I",
+              os.path.join(ROOT, "include"), os.path.join(HERE, "c", "owner_fuzz.c"), str(lib),
+              f"-Wl,-rpath,{tmp_path}", "-o", str(exe)])
+    assert r.returncode == 0, r.stderr[-2000:]
+    r = _run([str(exe), str(tmp_path / "owner.sock")], env=env)
+    assert r.returncode == 0 and "owner fuzz ok" in r.stdout, (r.stdout + r.stderr)[-3000:]
