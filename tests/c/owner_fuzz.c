@@ -5,7 +5,8 @@
  * times with random bytes, headers with random operations and lengths (most
  * announcing more payload than they send), descriptors passed with them, and
  * random commit payloads from a connection that holds the write lease; valid
- * clients of the C-ABI run the protocol in between.  Exits non-zero on any
+ * clients of the C-ABI run the protocol in between; then random calls with
+ * random leases on a host-only in-process store.  Exits non-zero on any
  * failed check; the sanitizers abort on any memory or UB error.
  */
 #define _GNU_SOURCE
@@ -183,6 +184,40 @@ int main(int argc, char **argv)
     }
     close(pipefd[0]);
     close(pipefd[1]);
+
+    /* the in-process store's protocol, host-only, under random calls with random leases: every
+     * call returns a status, and the reader count never exceeds the leases handed out */
+    gms_store *st = NULL;
+    CHECK(gms_store_create(GMS_HOST_ONLY, 0, 0, &st) == GMS_OK);
+    uint64_t leases[16] = {0};
+    int nl = 0;
+    for (int it = 0; it < 20000; ++it) {
+        uint64_t lease = 0, mm = 0, any = nl && rnd() % 4 ? leases[rnd() % (uint64_t)nl] : rnd() % 64;
+        int rc = GMS_OK;
+        switch (rnd() % 7) {
+        case 0: rc = gms_store_connect_rw(st, &lease); break;
+        case 1: rc = gms_store_connect_ro(st, rnd() % 2 ? GMS_CONNECT_VERIFY : 0, &lease, &mm, NULL); break;
+        case 2: rc = gms_store_commit(st, any, NULL, 0, NULL, &mm, NULL); break;
+        case 3: rc = gms_store_abort(st, any); break;
+        case 4: rc = gms_store_disconnect(st, any); break;
+        case 5: rc = gms_store_verify(st, &mm, NULL, 0, NULL); break;
+        default: {
+            uint64_t addr = 0;
+            rc = gms_store_alloc(st, any, 1 + rnd() % 4096, 0, &addr);
+            CHECK(rc != GMS_OK); /* a host-only store has no memory */
+        }
+        }
+        CHECK(rc <= 0 && rc >= GMS_ERR_INTEGRITY);
+        if (rc == GMS_OK && lease && nl < 16) leases[nl++] = lease;
+        int state = 0, inv = 0;
+        uint32_t rd = 0;
+        CHECK(gms_store_state(st, &state, &rd, &inv) == GMS_OK);
+        CHECK(state >= GMS_STORE_EMPTY && state <= GMS_STORE_RO && rd <= 16u + (uint32_t)it);
+        CHECK((state == GMS_STORE_RO) == (rd > 0));
+        if (nl == 16) nl = 0; /* forget old leases; the store keeps them */
+    }
+    gms_store_destroy(st);
+
     gms_owner_stop(o);
     CHECK(pthread_join(th, NULL) == 0);
     gms_owner_destroy(o);
