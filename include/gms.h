@@ -538,7 +538,8 @@ const uint64_t *gms_store_block_hashes(const gms_store *s);
  * process, on any stream, has landed), hashes every 4 KiB block of them (and compares with
  * expected_blk when given, refusing the commit on a mismatch with GMS_ERR_INTEGRITY while
  * the writer keeps its lease), and the owner records the layout and the hashes; the write
- * lease ends (the writer must not write after it).  A client's
+ * lease ends (the writer must not write after it) and the client's layout is emptied (as the
+ * paper's writer does, it reconnects read-only to use the committed state).  A client's
  * layout is the committed entries at its own addresses (gms_client_layout,
  * gms_client_manifest for gms_restore / gms_verify; empty before the first commit): a
  * reader's to use, a writer's to repopulate.  A writer that took over committed state gets

@@ -1170,6 +1170,7 @@ int gms_client_commit(gms_client *c, const gms_entry *entries, uint64_t n, const
     if (rc != GMS_OK) return rc;
     if (r.status != GMS_OK) return fail(r.status, "owner refused the commit");
     c->leased = false;  // the write lease ends at commit
+    drop_committed(c);  // the layout it took over is gone; a read-only reconnect gets the new one
     return GMS_OK;
 }
 

@@ -79,6 +79,7 @@ step("commit")
 entries = list(zip(addrs, sizes()))
 o_blk, _ = oracle.hashes(reference())
 c.commit(entries, expected=torch.from_numpy(o_blk.view(np.int64)).cuda())
+assert c.layout() == [] and c.manifest() is None  # the writer reconnects read-only to use it
 print("committed", json.dumps({"entries": len(entries), "info": c.info()}), flush=True)
 """
 
