@@ -232,3 +232,46 @@ def test_concurrent_host_threads_on_separate_manifests(tmp_path):
         back, whole = arena.read()
         assert all(np.array_equal(a, b) for a, b in zip(back, datas)) and arena.outside_untouched(whole)
         m.close()
+
+
+def test_two_threads_share_one_manifest_through_the_ring():
+    """Two host threads restore the same manifest from pinned images on their own streams, five
+    times each, with fused verification, while the library orders their use of the one staging
+    ring: a slot that one call overwrote under the other would show up as mismatching blocks.
+    The restored bytes equal the oracle's afterwards."""
+    import threading
+
+    need_gpu()
+    sizes = [int(v) for v in np.random.default_rng(91).integers(1, 5 << 20, 12)] + [(9 << 20) + 5, 4096]
+    arena, datas = _setup(sizes, seed=91)
+    m = gms.Manifest(arena.entries)
+    m.set_staging(1 << 20, 2)  # many 1 MiB slices through two slots
+    o_img = oracle.pack(datas)
+    o_blk, _ = oracle.hashes(datas)
+    exp = from_u64(o_blk)
+    images = [torch.from_numpy(o_img.copy()).pin_memory() for _ in range(2)]
+    streams = [torch.cuda.Stream() for _ in range(2)]
+    counts = [u64_dev(1) for _ in range(2)]
+    errors, seen = [], []
+
+    def work(k):
+        try:
+            for rep in range(5):
+                gms.restore(m, images[k], m.image_bytes, gms.MEM_HOST_PINNED, expected=exp,
+                            mismatch_count=counts[k], stream=streams[k])
+                streams[k].synchronize()
+                seen.append(int(to_u64(counts[k])[0]))
+        except BaseException as e:
+            errors.append((k, repr(e)))
+
+    threads = [threading.Thread(target=work, args=(k,)) for k in range(2)]
+    for t in threads:
+        t.start()
+    for t in threads:
+        t.join()
+    torch.cuda.synchronize()
+    assert not errors, errors
+    assert seen == [0] * 10, seen
+    back, whole = arena.read()
+    assert all(np.array_equal(a, b) for a, b in zip(back, datas)) and arena.outside_untouched(whole)
+    m.close()
