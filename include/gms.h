@@ -157,9 +157,9 @@ uint64_t gms_num_launch_groups(const gms_manifest *m);
 /* Launch group g (0 <= g < gms_num_launch_groups): its chunks, its work units per
  * chunk as a power of two (0: one unit per chunk, a paired launch), and flags:
  * GMS_GROUP_SHIFTED (entries off a 16-byte boundary, the byte-shifting kernels) and
- * GMS_GROUP_STRIPED (restores take the striped unit order: the group's chunks span
- * several work units and are mostly entries of their own, such as a KV pool's live
- * units).  Outputs may be NULL.
+ * GMS_GROUP_STRIPED (restores and snapshots take the striped unit order, as verify
+ * always does: the group's chunks span several work units and are mostly entries of
+ * their own, such as a KV pool's live units).  Outputs may be NULL.
  * Errors: GMS_ERR_INVALID (manifest null, g out of range). */
 enum gms_group_flags {
     GMS_GROUP_SHIFTED = 1,

@@ -188,9 +188,9 @@ void plan_launch_groups(gms_manifest *m)
         m->chunks.swap(sorted);
     }
     // A group whose chunks are mostly whole entries of their own (a KV pool's
-    // live units: destinations scattered over the pool) restores in the
-    // striped unit order; one of large tensors cut into many chunks keeps the
-    // contiguous eighths.  The chunks of an entry are adjacent in a group.
+    // live units: entries scattered over the pool) restores and snapshots in
+    // the striped unit order; one of large tensors cut into many chunks keeps
+    // the contiguous eighths.  The chunks of an entry are adjacent in a group.
     // Paired launches (one unit per chunk) keep their own order.
     for (LaunchGroup &lg : m->groups) {
         uint64_t entries = 0;

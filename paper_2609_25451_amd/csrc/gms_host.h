@@ -57,7 +57,7 @@ struct LaunchGroup {
     uint64_t first = 0, count = 0;
     uint32_t shift = 0;
     bool shifted = false;
-    bool striped = false;  // restore in the striped unit order (chunks of mostly separate entries)
+    bool striped = false;  // restore and snapshot in the striped unit order (chunks of mostly separate entries)
 };
 }  // namespace gms
 

@@ -11,7 +11,7 @@
 // launches reserve LDS so that six workgroups (12 waves) are resident per CU,
 // which measured best for the mixed read/write stream across weight sets,
 // shards and KV pools, and the unit order is XCD-aware (striped for verify and for
-// restores of scattered units, contiguous per XCD otherwise).  Hashing happens on
+// scattered units, contiguous per XCD otherwise).  Hashing happens on
 // the registers that were just moved: each lane mixes its eight 8-byte words,
 // the wave XOR-reduces its 64 partials with DPP row operations plus four lane
 // reads, and lane 0 stores / compares the block hash.  Tensor hashes combine
@@ -493,11 +493,11 @@ __device__ __forceinline__ uint64_t xcd_slot()
 // the entries together.  The last, partial round of stripes is split into eight
 // contiguous pieces, which keeps the order a permutation of the round's slots.
 // Measured on the llama8b set over six image allocations: 90.4 to 91.8% of HBM
-// peak against 86.8 to 88.8% with contiguous eighths.  Restores of launch groups
-// whose chunks are mostly entries of their own (`striped`, set by the manifest:
-// a KV pool's live units) take it too, 1.2 to 1.6 points above the eighths on
-// the KV pool; weight sets keep the eighths, where striping moved llama8b by
-// -1.0 to +0.0 points and the 70B shard by -2.9 to +1.5.  Snapshots keep them.
+// peak against 86.8 to 88.8% with contiguous eighths.  Restores and snapshots of
+// launch groups whose chunks are mostly entries of their own (`striped`, set by
+// the manifest: a KV pool's live units) take it too, 1.2 to 1.6 points above the
+// eighths on the KV pool for either; weight sets keep the eighths, where striping
+// moved llama8b by -1.0 to +0.0 points and the 70B shard by -2.9 to +1.5.
 constexpr uint64_t kVerifyStripe = 128;
 
 __device__ __forceinline__ uint64_t striped_slot()
@@ -512,7 +512,7 @@ __device__ __forceinline__ uint64_t striped_slot()
 // (2^shift units cover the launch's longest chunk); wave w of the workgroup
 // takes the unit's block w.  Tensor hashes combine the two waves' block
 // hashes in LDS and take one atomic XOR per unit.  `striped` (uniform) selects
-// the striped unit order for a restore.
+// the striped unit order for a restore or snapshot.
 template <int OP, bool HASH, bool SHIFTED>
 __global__ void __launch_bounds__(kUnitThreads)
 k_stream(const Chunk *__restrict__ chunks, uint64_t count, uint32_t unit_shift, gbyte *__restrict__ img_base,
@@ -525,7 +525,7 @@ k_stream(const Chunk *__restrict__ chunks, uint64_t count, uint32_t unit_shift, 
     const uint64_t *const exp_dummy = (const uint64_t *)chunks;  // any readable word
     const uint64_t units = count << unit_shift;
     const uint32_t unit_mask = (1u << unit_shift) - 1;
-    const uint64_t slot_in_round = OP == kVerify || (OP == kRestore && striped) ? striped_slot() : xcd_slot();
+    const uint64_t slot_in_round = OP == kVerify || striped ? striped_slot() : xcd_slot();
     for (uint64_t round = 0; round < units; round += gridDim.x) {
         const uint64_t u = round + slot_in_round;
         if (u >= units) break;  // uniform across the workgroup

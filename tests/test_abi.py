@@ -196,9 +196,9 @@ def test_launch_groups_split_only_when_idle_units_pay_for_a_launch():
     assert off[:4] == m1.layout()[0] and m.image_bytes == m1.image_bytes + 3000 * 4096
 
 
-def test_restores_of_scattered_units_take_the_striped_order():
+def test_scattered_units_take_the_striped_order():
     """A launch group whose chunks are mostly entries of their own (the KV pool's 64 KiB live
-    units) restores in the striped unit order; weight sets, whose tensors span many chunks,
+    units) restores and snapshots in the striped unit order; weight sets, whose tensors span many chunks,
     keep the contiguous eighths.  The query reports every group of a manifest."""
     p = synth.kv_pool()
     live = synth.live_map(p.blocks, p.n_live, p.map_seed, p.map_stream)
