@@ -3,12 +3,16 @@ sizes from 4 KiB to 1 MiB, entries at any byte alignment, sizes from one byte to
 mixes that split into paired and unit launches and into striped and contiguous unit orders,
 device images and pinned images through small staging rings.  Each case is the oracle round
 trip: snapshot image and hashes, a fused restore into poisoned memory with sentinels around
-every entry, and verify, all equal to the oracle."""
+every entry, and verify, all equal to the oracle; then bytes flipped at random image offsets
+(payload or padding) and a second fused restore, whose mismatch count and list equal the
+oracle's verify of the corrupted image unpacked."""
 import numpy as np
 import pytest
+import torch
 
+import oracle
 import paper_2609_25451_amd as gms
-from gpu_util import Arena, need_gpu, random_datas
+from gpu_util import Arena, from_u64, need_gpu, random_datas, to_u64, u64_dev
 from test_gpu_parity import _round_trip
 
 pytestmark = pytest.mark.gpu
@@ -48,8 +52,30 @@ def test_random_manifest_round_trip(seed):
     datas = random_datas(sizes, seed=3000 + seed)
     arena.fill(datas)
     staging = (max(chunk, 1 << 20), 2) if pinned else None
-    m, _ = _round_trip(arena, datas, gms.MEM_HOST_PINNED if pinned else gms.MEM_DEVICE, chunk_bytes=chunk,
+    m, img = _round_trip(arena, datas, gms.MEM_HOST_PINNED if pinned else gms.MEM_DEVICE, chunk_bytes=chunk,
                        staging=staging)
     groups = m.launch_groups()
     assert sum(g["chunks"] for g in groups) == m.num_chunks
+
+    # corruption: flip bytes anywhere in the image, padding included (padding is neither
+    # restored nor hashed, so a flip there must flag nothing)
+    rng = np.random.default_rng(4000 + seed)
+    host = img.cpu().numpy()[: m.image_bytes].copy() if not pinned else img.numpy()[: m.image_bytes]
+    for pos in rng.integers(0, m.image_bytes, int(rng.integers(1, 6))):
+        host[pos] ^= np.uint8(1 << int(rng.integers(0, 8)))
+    if not pinned:
+        img[: m.image_bytes].copy_(torch.from_numpy(host))
+    bad = oracle.unpack(host, sizes)
+    o_blk, _ = oracle.hashes(datas)
+    o_cnt, o_lst = oracle.verify(bad, o_blk)
+    arena.poison()
+    cnt, lst = u64_dev(1), u64_dev(16)
+    gms.restore(m, img, m.image_bytes, gms.MEM_HOST_PINNED if pinned else gms.MEM_DEVICE, expected=from_u64(o_blk),
+                mismatch_count=cnt, mismatch_list=lst, mismatch_cap=16)
+    torch.cuda.synchronize()
+    back, _ = arena.read()
+    assert all(np.array_equal(a, b) for a, b in zip(back, bad))
+    got = int(to_u64(cnt)[0])
+    assert got == o_cnt
+    assert sorted(to_u64(lst)[: min(got, 16)].tolist()) == o_lst[:16].tolist()
     m.close()
