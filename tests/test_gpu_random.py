@@ -3,7 +3,8 @@ sizes from 4 KiB to 1 MiB, entries at any byte alignment, sizes from one byte to
 mixes that split into paired and unit launches and into striped and contiguous unit orders,
 device images and pinned images through small staging rings.  Each case is the oracle round
 trip: snapshot image and hashes, a fused restore into poisoned memory with sentinels around
-every entry, and verify, all equal to the oracle; then bytes flipped at random image offsets
+every entry, and verify, all equal to the oracle; the same restore from ordinary host memory
+and through the allocation-free path in slices of a random number of chunks; then bytes flipped at random image offsets
 (payload or padding) and a second fused restore, whose mismatch count and list equal the
 oracle's verify of the corrupted image unpacked."""
 import numpy as np
@@ -45,6 +46,7 @@ def _case(seed):
 def test_random_manifest_round_trip(seed):
     need_gpu()
     sizes, p_mis, chunk, pinned = _case(1000 + seed)
+    rng_slices = np.random.default_rng(5000 + seed)
     print(f"case {seed}: {len(sizes)} entries, {sum(sizes)} B, chunk {chunk}, misaligned {p_mis}, "
           f"pinned {pinned}", flush=True)
     arena = Arena(sizes, misalign=lambda r: r.integers(1, 16) if r.random() < p_mis else 0, gap=24,
@@ -56,6 +58,31 @@ def test_random_manifest_round_trip(seed):
                        staging=staging)
     groups = m.launch_groups()
     assert sum(g["chunks"] for g in groups) == m.num_chunks
+    o_img = oracle.pack(datas)
+    o_blk, o_ten = oracle.hashes(datas)
+    exp = from_u64(o_blk)
+
+    def check(restore_call, what):
+        arena.poison()
+        blk, ten, cnt = u64_dev(m.num_blocks), u64_dev(m.num_entries), u64_dev(1)
+        restore_call(blk, ten, cnt)
+        torch.cuda.synchronize()
+        back, whole = arena.read()
+        assert all(np.array_equal(a, b) for a, b in zip(back, datas)), what
+        assert arena.outside_untouched(whole), what
+        assert int(to_u64(cnt)[0]) == 0, what
+        assert np.array_equal(to_u64(blk, m.num_blocks), o_blk) and np.array_equal(to_u64(ten, m.num_entries), o_ten)
+
+    # the same image from ordinary host memory (pieces through the host and device rings) ...
+    m.set_staging(max(chunk, 1 << 20), 2)
+    check(lambda blk, ten, cnt: gms.restore_from_host(m, o_img, expected=exp, blk_hash=blk, ten_hash=ten,
+                                                      mismatch_count=cnt), "pageable host image")
+    # ... and pinned through the fixed staging area, in slices of a random number of chunks
+    pin = torch.from_numpy(o_img.copy()).pin_memory()
+    slice_bytes = chunk * int(rng_slices.integers(1, max(2, gms.NOALLOC_STAGING_BYTES // chunk // 8)))
+    check(lambda blk, ten, cnt: gms.restore_pinned_noalloc(m, pin, staging_bytes=slice_bytes, expected=exp,
+                                                           blk_hash=blk, ten_hash=ten, mismatch_count=cnt),
+          f"allocation-free restore, {slice_bytes} B slices")
 
     # corruption: flip bytes anywhere in the image, padding included (padding is neither
     # restored nor hashed, so a flip there must flag nothing)
