@@ -4,7 +4,8 @@ mixes that split into paired and unit launches and into striped and contiguous u
 device images and pinned images through small staging rings.  Each case is the oracle round
 trip: snapshot image and hashes, a fused restore into poisoned memory with sentinels around
 every entry, and verify, all equal to the oracle; the same restore from ordinary host memory
-and through the allocation-free path in slices of a random number of chunks; then bytes flipped at random image offsets
+and through the allocation-free path in slices of a random number of chunks, and for every fourth
+case from an image file; then bytes flipped at random image offsets
 (payload or padding) and a second fused restore, whose mismatch count and list equal the
 oracle's verify of the corrupted image unpacked."""
 import numpy as np
@@ -43,7 +44,7 @@ def _case(seed):
 
 
 @pytest.mark.parametrize("seed", range(24))
-def test_random_manifest_round_trip(seed):
+def test_random_manifest_round_trip(seed, tmp_path):
     need_gpu()
     sizes, p_mis, chunk, pinned = _case(1000 + seed)
     rng_slices = np.random.default_rng(5000 + seed)
@@ -83,6 +84,18 @@ def test_random_manifest_round_trip(seed):
     check(lambda blk, ten, cnt: gms.restore_pinned_noalloc(m, pin, staging_bytes=slice_bytes, expected=exp,
                                                            blk_hash=blk, ten_hash=ten, mismatch_count=cnt),
           f"allocation-free restore, {slice_bytes} B slices")
+    if seed % 4 == 0:  # an image file at an offset, direct or buffered, with a random worker count
+        path = tmp_path / "image.bin"
+        off = 4096 * int(rng_slices.integers(0, 4))
+        with open(path, "wb") as f:
+            f.write(b"\0" * off)
+            f.write(o_img.tobytes())
+        flags = gms.FILE_DIRECT if seed % 8 == 0 else 0
+        threads = int(rng_slices.integers(1, 9))
+        check(lambda blk, ten, cnt: gms.restore_from_file(m, path, file_offset=off, flags=flags, io_threads=threads,
+                                                          expected=exp, blk_hash=blk, ten_hash=ten,
+                                                          mismatch_count=cnt),
+              f"image file, offset {off}, flags {flags}, {threads} workers")
 
     # corruption: flip bytes anywhere in the image, padding included (padding is neither
     # restored nor hashed, so a flip there must flag nothing)
