@@ -157,6 +157,49 @@ c.commit(list(zip(addrs, sizes())), expected=torch.from_numpy(o_blk.view(np.int6
 print("reshaped", flush=True)
 """
 
+_ALLOCATOR = _COMMON + r"""
+# a writer's first-fit suballocation under a random walk of allocs and frees: live parts never
+# overlap, each holds its own bytes after every other part was written, and the live set
+# commits and verifies in a reader
+rng = np.random.default_rng(int(sys.argv[3]))
+c = gms.Client(SOCK, gms.LEASE_RW)
+live = {}  # addr -> (bytes, stream id)
+sid = 10
+for step in range(300):
+    if live and rng.random() < 0.4:
+        a = list(live)[int(rng.integers(0, len(live)))]
+        c.free(a)
+        del live[a]
+        continue
+    r = rng.random()
+    if r < 0.6:
+        n = int(rng.integers(1, 5000))
+    elif r < 0.9:
+        n = int(rng.integers(5000, 3 << 20))
+    elif r < 0.97:
+        n = int(rng.integers(300 << 20, 520 << 20))  # up to about half a slab: first fit
+    else:
+        n = int(rng.integers(600 << 20, 1 << 30))  # an allocation of its own
+    align = int(rng.choice([0, 16, 256, 4096]))
+    a = c.alloc(n, align=align)
+    assert align == 0 or a % align == 0
+    for b, (m, _) in live.items():
+        assert a + n <= b or b + m <= a, ("overlap", a, n, b, m)
+    sid += 1
+    live[a] = (n, sid)
+for a, (n, k) in live.items():
+    synth.dev_fill_bytes(a, n, 5, k)
+torch.cuda.synchronize()
+entries = sorted((a, n) for a, (n, _) in live.items())
+datas = [synth.random_bytes(n, 5, live[a][1]) for a, n in entries]
+for (a, n), want in zip(entries, datas):
+    if n <= (8 << 20):
+        assert np.array_equal(d2h(a, n), want), "a part was overwritten by another"
+o_blk, _ = oracle.hashes(datas)
+c.commit(entries, expected=torch.from_numpy(o_blk.view(np.int64)).cuda())
+print("allocator ok", len(entries), flush=True)
+"""
+
 _CORRUPTER = _COMMON + r"""
 # stands for a fault that changes committed memory behind the protocol's back: this reader
 # writes one byte of entry 3 through its own mapping (nothing in the library would)
@@ -335,3 +378,16 @@ def test_writer_takes_over_committed_slabs_frees_and_reallocates(owner):
     assert "reshaped" in _finish(_spawn(_RESHAPER, owner))
     assert gms.owner_query(owner)[:3] == ("COMMITTED", 0, False) and gms.owner_query(owner)[3] == allocs
     _finish(_spawn(_READER, owner))
+
+
+def test_writer_suballocation_random_walk(owner):
+    """300 random allocs and frees (bytes to 1 GiB, alignments to 4 KiB) in a writer process:
+    no two live parts overlap, every part keeps its own bytes, and the surviving set commits
+    against the oracle's hashes and verifies in a reader."""
+    print("allocating writer", flush=True)
+    out = _finish(_spawn(_ALLOCATOR, owner, "7"))
+    assert "allocator ok" in out
+    assert gms.owner_query(owner)[:3] == ("COMMITTED", 0, False)
+    c = gms.Client(owner, gms.LEASE_RO, verify=True)  # re-hashed here against the commit-time hashes
+    assert c.verify() == 0
+    c.close()
