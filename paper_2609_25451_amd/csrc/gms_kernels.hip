@@ -235,6 +235,15 @@ __device__ __forceinline__ void store_block(const u32x4 v[4], gbyte *p)
     for (int k = 0; k < 4; ++k) __builtin_nontemporal_store(v[k], (gvec *)(p + k * 1024));
 }
 
+// A snapshot wave pauses about 512 cycles after storing its block, before it
+// hashes or exits.  The image it writes is one contiguous stream, and without
+// the pause the next workgroup's gather reads start while that stream's
+// stores are still in flight: an unhashed snapshot of the llama8b set read
+// 78.5 to 79.3% of HBM peak without it and 80.4 to 81.3% with a pause of 128 to
+// 2048 cycles; with hashes, 81.2 to 81.5% without and 81.7% at 512 cycles
+// (79.9% at 2048).  Restores gained nothing from it.
+constexpr int kSnapshotPause = 8;  // s_sleep units of 64 cycles
+
 // An interior block of the shifted path (see move_block_shifted): a restore's
 // full block that is not its chunk's last, or any full block of a snapshot or
 // verify.  Every granule is whole (bar a chunk's first, for a restore), so no
@@ -280,6 +289,7 @@ __device__ __forceinline__ uint64_t interior_block(uint32_t b, gbyte *img, gbyte
             seg[k] = join_at<D>(g[k], next, r);
             if (OP == kSnapshot) __builtin_nontemporal_store(seg[k], (gvec *)(img + k * 1024));
         }
+        if (OP == kSnapshot) __builtin_amdgcn_s_sleep(kSnapshotPause);
     }
     uint64_t tacc = 0;
     if (HASH) {
@@ -415,15 +425,6 @@ __device__ __forceinline__ uint64_t move_block_shifted(const Chunk &c, uint32_t 
     }
     return tacc;
 }
-
-// A snapshot wave pauses about 512 cycles after storing its block, before it
-// hashes or exits.  The image it writes is one contiguous stream, and without
-// the pause the next workgroup's gather reads start while that stream's
-// stores are still in flight: an unhashed snapshot of the llama8b set read
-// 78.5 to 79.3% of HBM peak without it and 80.4 to 81.3% with a pause of 128 to
-// 2048 cycles; with hashes, 81.2 to 81.5% without and 81.7% at 512 cycles
-// (79.9% at 2048).  Restores gained nothing from it.
-constexpr int kSnapshotPause = 8;  // s_sleep units of 64 cycles
 
 // Block b of chunk c, by one wave.  Chunks of entries at a 16-byte-aligned
 // address (SHIFTED false; launches never mix the two kinds) move a full block
