@@ -279,7 +279,10 @@ def main():
         with GpuSampler() as gs:
             t = settled(timer, lambda: gms.snapshot(m, image, m.image_bytes, gms.MEM_DEVICE, blk_hash=blk2))
         assert torch.equal(blk2, expected)
-        result_rows["snapshot_d2d_hash"] = {"s": t, "GB_s": P / t / 1e9, "hbm_frac": 2 * P / t / 1e9 / HBM_PEAK_GBS,
+        tp = settled(timer, lambda: gms.snapshot(m, image, m.image_bytes, gms.MEM_DEVICE))  # no hashes
+        result_rows["snapshot_d2d_hash"] = {"s": t, "GB_s": P / t / 1e9,
+                                            "hbm_frac": (2 * P + 8 * nb) / t / 1e9 / HBM_PEAK_GBS,
+                                            "unhashed_s": tp, "unhashed_hbm_frac": 2 * P / tp / 1e9 / HBM_PEAK_GBS,
                                             "gpu": gs.summary()}
     if "plain" in rows:
         with GpuSampler() as gs:
